@@ -1,0 +1,193 @@
+"""Benchmark of the TReVS pruning hot path on one MI355X.
+
+One step = stage 1 (trevs_prellm_prune) + stage 2 (trevs_inllm_prune) over one
+batch of synthetic inputs already resident in HBM.  Prints ONE JSON line with
+the throughput in visual tokens per second (B*N input visual tokens carried
+through both stages per step), the roofline record of the dominant kernel
+(the textual-relevance stream of stage 1, timed live with HIP events on the
+launch stream), and the CPU oracle's rate on a bounded sample of the same
+workload."""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "visual tokens scored+pruned/sec (both stages) at 1 MI355X; % of HBM roofline"
+
+
+def algorithmic_bytes(w, text_len):
+    """Bytes the method must move per step (every input read once, every
+    output written once) and per launch of the relevance kernel."""
+    e = w.elem_bytes
+    B = w.B
+    m_bar = float(np.mean(text_len))
+    rel = B * (e * (w.H_v * w.N + w.N * w.d + m_bar * w.d) + 8 * w.N)
+    stage1 = B * e * (w.H_v * w.N + w.N * w.d + m_bar * w.d + 2 * w.K1 * w.d) + 4 * B * w.K1
+    So = w.S - w.K1 + w.K2
+    stage2 = (B * e * (m_bar * w.H_q * w.d_h + w.K1 * w.H_kv * w.d_h)
+              + B * (2 * So * w.D * e + 4 * So * w.H_kv * w.d_h * e + 2 * w.n_pos * So * 8 + 4 * w.K2))
+    return dict(relevance=rel, stage1=stage1, stage2=stage2, total=stage1 + stage2)
+
+
+def cpu_baseline(w, s1, s2, budget_s):
+    """The CPU oracle as it stands, on single samples of the same workload,
+    repeated until about budget_s seconds of work."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        b = n % w.B
+        oracle.prellm(s1["cls_logits"][b:b + 1], s1["vis_feats"][b:b + 1], s1["text_emb"][b:b + 1],
+                      s1["text_len"][b:b + 1], w.dtype, n_seg=w.n_seg, k_keep=w.K1, rho=w.rho)
+        oracle.inllm(s2["q"][b:b + 1], s2["k"][b:b + 1], s2["v"][b:b + 1], s2["hidden"][b:b + 1],
+                     s2["pos"][:, b:b + 1], s2["text_len"][b:b + 1], w.dtype, P=w.P, K1=w.K1,
+                     n_keep=w.n_keep, k_keep=w.K2, scale=1.0 / math.sqrt(w.d_h))
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or n >= 4 * w.B:
+            break
+    return {"value": n * w.N / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} single samples (B=1) of {w.name}, both stages, float64 NumPy, "
+                      f"{el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the pruning path "
+              "shards by sample across GPUs with no exchange, so run one process per GPU.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_37581_amd import trevs
+    from synthetic import DEFAULT_BENCH_WORKLOAD, WORKLOADS, stage1_inputs, stage2_inputs
+
+    w = WORKLOADS[args.workload or DEFAULT_BENCH_WORKLOAD]
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
+    s1 = stage1_inputs(w)
+    s2 = stage2_inputs(w)
+
+    def to_dev(a):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        return (t.view(torch.bfloat16) if t.dtype == torch.uint16 else t).to(dev)
+
+    cls, Z, T = to_dev(s1["cls_logits"]), to_dev(s1["vis_feats"]), to_dev(s1["text_emb"])
+    tl = to_dev(s1["text_len"])
+    q, k, v, hid, pos = (to_dev(s2[x]) for x in ("q", "k", "v", "hidden", "pos"))
+    tl2 = to_dev(s2["text_len"])
+    pre = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, n_seg=w.n_seg, textual_ratio=w.rho)
+    inl = trevs.Inllm(q, k, v, hid, pos, tl2, P=w.P, K_in=w.K1, n_keep_heads=w.n_keep,
+                      k_keep=w.K2)
+    stream = torch.cuda.current_stream()
+    n1, n2 = 2 * trevs.PRELLM_NUM_KERNELS, 2 * trevs.INLLM_NUM_KERNELS
+    ev = trevs.HipEvents(args.steps * (n1 + n2))
+
+    def step(i=None):
+        if i is None:
+            pre(stream)
+            inl(stream)
+        else:
+            base = i * (n1 + n2)
+            pre(stream, events=ev.handles[base:base + n1])
+            inl(stream, events=ev.handles[base + n1:base + n1 + n2])
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        step(i)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = start.elapsed_time(stop) / args.steps
+    names = [f"prellm.{n}" for n in trevs.PRELLM_KERNELS] + [f"inllm.{n}" for n in trevs.INLLM_KERNELS]
+    kern_ms = {n: 0.0 for n in names}
+    for i in range(args.steps):
+        base = i * (n1 + n2)
+        for j, n in enumerate(names):
+            kern_ms[n] += ev.elapsed_ms(base + 2 * j, base + 2 * j + 1) / args.steps
+    ev.close()
+    print(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # device copy bandwidth of the same run (context, and the reference kernel
+    # for scaling the HBM counters of a profile)
+    nbytes = 1 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(5):
+        dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbps = 2 * nbytes * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
+
+    nb = algorithmic_bytes(w, s1["text_len"])
+    rel_s = kern_ms["prellm.relevance"] * 1e-3
+    achieved = nb["relevance"] / rel_s / 1e9
+    t_step = ms_step * 1e-3
+    tokens = w.B * w.N
+    result = {
+        "metric": METRIC,
+        "value": tokens / t_step,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "N": w.N, "d": w.d, "M_max": w.M_max,
+                   "K1": w.K1, "K2": w.K2, "H_q": w.H_q, "H_kv": w.H_kv, "d_head": w.d_h,
+                   "D": w.D, "n_keep_heads": w.n_keep, "P": w.P, "S": w.S},
+        "roofline": {"bound": "hbm", "kernel": "prellm.relevance", "achieved": achieved,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": None, "bytes_per_launch": nb["relevance"]},
+        "path_hbm_frac": nb["total"] / t_step / 1e9 / HBM_PEAK_GBPS,
+        "path_bytes": nb,
+        "kernels_us": {n: round(v * 1e3, 3) for n, v in kern_ms.items()},
+        "copy_gbps": copy_gbps,
+        "wall_s": t_wall,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, s1, s2, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

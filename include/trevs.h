@@ -1,0 +1,195 @@
+/*
+ * trevs.h - C ABI of the TReVS visual-token pruning library for MI355X (gfx950).
+ *
+ * TReVS ("Integrating Textual Relevance and Visual Saliency for Efficient
+ * Vision-Language Model Token Pruning", arxiv 2609.37581) prunes the visual
+ * tokens of a vision-language model in two stages:
+ *   Stage 1, before the LLM (Sec. 4.1, Eq. (2)-(7)): fuse the vision
+ *     encoder's [CLS] attention saliency with the textual relevance of each
+ *     visual token, take a stable top-K_1, and gather the kept tokens.
+ *   Stage 2, inside the LLM at one layer (Sec. 4.2, Eq. (8)-(9)): compute the
+ *     text->vision attention, keep the high-variance heads, score each visual
+ *     token by its max-over-text attention averaged over those heads, take a
+ *     stable top-K_2, and compact hidden states, position ids and K/V rows.
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE pointers to dense row-major tensors.  Float
+ *     tensors share one element type per call (trevs_dtype).  Pointers that
+ *     are read or written as 16-byte vectors (named below) must be 16-byte
+ *     aligned; every other tensor must be aligned to its element size.
+ *   - The caller owns every buffer, including the workspace; the library
+ *     never allocates, frees or keeps state between calls.  Calls are
+ *     reentrant and thread-safe.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL means
+ *     the default stream); the host never waits for the device.
+ *   - Arguments are validated on the host before anything is launched;
+ *     invalid arguments return an error and launch nothing.  Values that live
+ *     in device memory (text lengths) cannot be checked without a device
+ *     synchronisation: out-of-range values there are undefined behaviour.
+ *   - Inputs must be finite.  Output buffers must not overlap the inputs or
+ *     each other.  Outputs are undefined when an error is returned.
+ *   - Index lists are int32, ascending and unique.  Top-K order is score
+ *     descending with ties going to the lower index.
+ *   - Optional `events`: NULL, or an array of 2*TREVS_*_NUM_KERNELS
+ *     hipEvent_t handles (entries may be NULL).  Event 2k is recorded on the
+ *     stream right before kernel k of the call and event 2k+1 right after
+ *     it, for per-kernel timing by the caller.
+ */
+#ifndef TREVS_H
+#define TREVS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum trevs_status {
+  TREVS_OK = 0,
+  TREVS_ERR_INVALID_ARG = 1, /* a size, ratio, pointer or alignment is invalid */
+  TREVS_ERR_UNSUPPORTED = 2, /* valid, but beyond this implementation's limits */
+  TREVS_ERR_WORKSPACE = 3,   /* workspace NULL, misaligned or too small */
+  TREVS_ERR_HIP = 4          /* a HIP launch or event call failed */
+} trevs_status;
+
+typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
+
+/* Implementation limits (TREVS_ERR_UNSUPPORTED beyond them). */
+#define TREVS_MAX_SELECT_N 32768 /* tokens ranked per sample by one top-K */
+#define TREVS_PRELLM_NUM_KERNELS 4 /* prep, relevance, select, gather */
+#define TREVS_INLLM_NUM_KERNELS 5  /* t2v stats, head select, token score, top-K, compaction */
+
+/* ------------------------------------------------------------------------
+ * Stage 1 (pre-LLM), Sec. 4.1.  Per sample b:
+ *   s^v_i  = (1/H_v) sum_h softmax(cls_logits[b,h,segment(i)])[i]   Eq. (2)-(3)
+ *            the softmax runs over the N/n_seg patch logits of the segment
+ *            (image tile or video frame) holding patch i.
+ *   s^t_i  = sqrt((1/M_b) sum_{j<M_b} max(tbar_j . zbar_i, 0)^2)     Eq. (4)-(5)
+ *            zbar, tbar: rows of vis_feats / text_emb over their L2 norm
+ *            (norm floored at 1e-12); M_b = text_len[b].
+ *   shat^c = max((s^c - Med(s^c)) / (MAD(s^c) + eps), 0) / tau_c     Eq. (6)
+ *            Med = lower median (0-based rank floor((N-1)/2)), MAD = lower
+ *            median of |s^c - Med|.
+ *   s_i    = max(a_i, b_i) + lambda sqrt(a_i b_i),                   Eq. (7)
+ *            a = 2(1-rho) shat^v, b = 2 rho shat^t  (rho = textual_ratio;
+ *            rho = 0.5 is Eq. (7) exactly, rho = 0 is [CLS]-only saliency).
+ *   kept_idx[b]   = TopK(s, k_keep) in ascending order
+ *   kept_feats[b] = vis_feats[b, kept_idx[b], :]  (bit copy)
+ * ---------------------------------------------------------------------- */
+typedef struct trevs_prellm_args {
+  uint32_t struct_size;      /* sizeof(trevs_prellm_args) */
+  int32_t B;                 /* samples */
+  int32_t N;                 /* visual tokens per sample, 1..TREVS_MAX_SELECT_N */
+  int32_t n_seg;             /* [CLS] softmax segments; N % n_seg == 0 */
+  int32_t H_v;               /* vision-encoder heads, >= 1 */
+  int32_t d;                 /* projected width d'; d * elem_size % 16 == 0 */
+  int32_t M_max;             /* padded text rows, >= 1 */
+  int32_t k_keep;            /* K_1 = K_r + K_d, 1..N */
+  int32_t k_div;             /* K_d (farthest-point diversity set); must be 0 */
+  float textual_ratio;       /* rho in [0, 1]; 0.5 reproduces Eq. (7) */
+  float tau_v, tau_t;        /* temperatures > 0 (paper: 1.4, 1.0) */
+  float lambda_;             /* consistency reward weight >= 0 (paper: 1.0) */
+  float eps;                 /* MAD stabiliser >= 0 (default 1e-8) */
+  int32_t dtype;             /* trevs_dtype of cls_logits, vis_feats, text_emb, kept_feats */
+  const void* cls_logits;    /* [B,H_v,N] pre-softmax [CLS]->patch logits, scaled by 1/sqrt(d_h) */
+  const void* vis_feats;     /* [B,N,d] projected visual features Z (16-byte aligned) */
+  const void* text_emb;      /* [B,M_max,d] text embeddings (16-byte aligned) */
+  const int32_t* text_len;   /* [B] valid text rows M_b in 1..M_max, or NULL (= M_max) */
+  int32_t* kept_idx;         /* OUT [B,k_keep] ascending */
+  void* kept_feats;          /* OUT [B,k_keep,d] gathered rows (16-byte aligned) */
+  float* score_out;          /* OPTIONAL OUT [B,N] fused score s */
+  float* sal_out;            /* OPTIONAL OUT [B,N] s^v */
+  float* rel_out;            /* OPTIONAL OUT [B,N] s^t */
+  float* norm_stats;         /* OPTIONAL OUT [B,4] Med(s^v), MAD(s^v), Med(s^t), MAD(s^t) */
+  void* const* events;       /* OPTIONAL [2*TREVS_PRELLM_NUM_KERNELS] hipEvent_t */
+} trevs_prellm_args;
+
+/* ------------------------------------------------------------------------
+ * Stage 2 (in-LLM, at the pruning layer), Sec. 4.2.  Sequence layout per
+ * sample: rows [0,P) prefix, [P,P+K_in) visual, [P+K_in, P+K_in+T_max) text,
+ * then any further rows up to S.  Per sample b with G = H_q/H_kv and
+ * T_b = text_len[b]:
+ *   x[h,q,i] = scale * q[b,P+K_in+q,h,:] . k[b,P+i,h/G,:]   (q < T_b, i < K_in)
+ *   A[h,q,:] = exp(x[h,q,:] - LSE[h,q]), LSE = logsumexp_i x[h,q,i], or, when
+ *              lse_rest is given, logaddexp(that, lse_rest[b,h,q]): the
+ *              full-row softmax restricted to the visual columns.
+ *   u_h      = (1/T_b) sum_q Var_i A[h,q,i]  (population variance)    Eq. (8)
+ *   H*       = the n_keep_heads heads first under (u desc, h asc)
+ *   p_i      = max_{q<T_b} (1/|H*|) sum_{h in H*} A[h,q,i]            Eq. (9)
+ *   kept_idx = TopK(p, k_keep) ascending, relative to the visual block
+ *   rows     = [0,P) ++ (P + kept_idx) ++ [P+K_in, S);  S' = S - K_in + k_keep
+ *   hidden_out[b] = hidden[b,rows], k_out[b] = k[b,rows], v_out[b] = v[b,rows],
+ *   pos_out[p,b]  = pos[p,b,rows]   (bit copies; position ids are not renumbered)
+ * ---------------------------------------------------------------------- */
+typedef struct trevs_inllm_args {
+  uint32_t struct_size;      /* sizeof(trevs_inllm_args) */
+  int32_t B;                 /* samples */
+  int32_t S;                 /* sequence rows at the pruning layer */
+  int32_t P;                 /* prefix rows before the visual block, >= 0 */
+  int32_t K_in;              /* visual rows K_1, 1..TREVS_MAX_SELECT_N */
+  int32_t T_max;             /* padded text rows; P + K_in + T_max <= S */
+  int32_t H_q, H_kv;         /* query / key-value heads; H_q % H_kv == 0 */
+  int32_t d_head;            /* 64, 128 or 256 */
+  int32_t D;                 /* hidden size; D * elem_size % 16 == 0 */
+  int32_t n_pos;             /* position-id planes (1, or 3 for M-RoPE), >= 1 */
+  int32_t n_keep_heads;      /* |H*|, 1..H_q (paper: H_q / 2) */
+  int32_t k_keep;            /* K_2, 1..K_in */
+  float scale;               /* logit scale > 0, normally 1/sqrt(d_head) */
+  int32_t dtype;             /* trevs_dtype of q, k, v, hidden and their outputs */
+  const void* q;             /* [B,S,H_q,d_head] (16-byte aligned) */
+  const void* k;             /* [B,S,H_kv,d_head] (16-byte aligned) */
+  const void* v;             /* [B,S,H_kv,d_head] (16-byte aligned) */
+  const void* hidden;        /* [B,S,D] (16-byte aligned) */
+  const int64_t* pos;        /* [n_pos,B,S] */
+  const int32_t* text_len;   /* [B] T_b in 1..T_max, or NULL (= T_max) */
+  const float* lse_rest;     /* OPTIONAL [B,H_q,T_max] log-sum-exp of each text row's non-visual logits */
+  int32_t* kept_idx;         /* OUT [B,k_keep] ascending, relative to the visual block */
+  void* hidden_out;          /* OUT [B,S',D] (16-byte aligned) */
+  void* k_out;               /* OUT [B,S',H_kv,d_head] (16-byte aligned) */
+  void* v_out;               /* OUT [B,S',H_kv,d_head] (16-byte aligned) */
+  int64_t* pos_out;          /* OUT [n_pos,B,S'] */
+  int32_t* head_sel;         /* OPTIONAL OUT [B,n_keep_heads] H*, ascending */
+  float* head_var;           /* OPTIONAL OUT [B,H_q] u_h */
+  float* score_out;          /* OPTIONAL OUT [B,K_in] p_i */
+  void* const* events;       /* OPTIONAL [2*TREVS_INLLM_NUM_KERNELS] hipEvent_t */
+} trevs_inllm_args;
+
+/* Workspace bytes the call needs for these arguments (0 on invalid args).
+ * The workspace must be 256-byte aligned; its contents need no initialisation
+ * and are garbage afterwards. */
+size_t trevs_prellm_workspace_size(const trevs_prellm_args* args);
+size_t trevs_inllm_workspace_size(const trevs_inllm_args* args);
+size_t trevs_topk_workspace_size(int32_t B, int32_t N, int32_t K);
+
+/* Stage 1 (Sec. 4.1, Eq. (2)-(7) and the pivot Top-K). */
+trevs_status trevs_prellm_prune(const trevs_prellm_args* args, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/* Stage 2 (Sec. 4.2, Eq. (8)-(9), Top-K_2 and compaction). */
+trevs_status trevs_inllm_prune(const trevs_inllm_args* args, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* Stable top-K of each row of scores [B,N] (device, finite fp32): writes the
+ * K kept indices of row b, ascending, to kept_idx [B,K].  N in
+ * 1..TREVS_MAX_SELECT_N, K in 1..N.  Needs no workspace (pass NULL, 0). */
+trevs_status trevs_topk_select(const float* scores, int32_t B, int32_t N, int32_t K,
+                               int32_t* kept_idx, void* workspace, size_t workspace_bytes,
+                               void* stream);
+
+/* Static description of a status code. */
+const char* trevs_status_string(trevs_status status);
+
+/* Budget bookkeeping: floor(ratio * n + 1/2) clamped to [1, n] (0 if n < 1). */
+int32_t trevs_keep_count(float ratio, int32_t n);
+
+/* sizeof() of the argument structs as compiled into the library, for
+ * bindings that mirror them. */
+size_t trevs_prellm_args_size(void);
+size_t trevs_inllm_args_size(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREVS_H */

@@ -1,0 +1,474 @@
+// Host side of the C ABI: argument validation, workspace layout and the
+// launch sequence of each stage.  Nothing here allocates device memory or
+// waits for the device.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "../../include/trevs.h"
+#include "common.hpp"
+#include "kernels.hpp"
+
+using namespace trevs;
+
+namespace {
+
+constexpr size_t kWsAlign = 256;
+
+size_t align_up(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+bool finite(float x) { return isfinite(x) != 0; }
+int elem_bytes(int dtype) { return dtype == TREVS_BF16 ? 2 : 4; }
+
+struct Span {
+  const void* p;
+  size_t n;
+};
+bool overlap(Span a, Span b) {
+  if (!a.p || !b.p || a.n == 0 || b.n == 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+  return a0 < b0 + b.n && b0 < a0 + a.n;
+}
+// Every output span must be disjoint from every input span and from the
+// other outputs.
+bool any_overlap(const Span* out, int n_out, const Span* in, int n_in) {
+  for (int i = 0; i < n_out; ++i) {
+    for (int j = 0; j < n_in; ++j)
+      if (overlap(out[i], in[j])) return true;
+    for (int j = i + 1; j < n_out; ++j)
+      if (overlap(out[i], out[j])) return true;
+  }
+  return false;
+}
+
+trevs_status record(void* const* events, int slot, hipStream_t s) {
+  if (events && events[slot]) {
+    if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[slot]), s) != hipSuccess) return TREVS_ERR_HIP;
+  }
+  return TREVS_OK;
+}
+
+// ------------------------------------------------------------------ stage 1
+struct PrellmLayout {
+  size_t row_stats, inv_tnorm, sal, rel, total;
+};
+
+trevs_status validate_prellm(const trevs_prellm_args* a) {
+  if (!a || a->struct_size != sizeof(trevs_prellm_args)) return TREVS_ERR_INVALID_ARG;
+  if (a->dtype != TREVS_F32 && a->dtype != TREVS_BF16) return TREVS_ERR_INVALID_ARG;
+  if (a->B < 1 || a->N < 1 || a->n_seg < 1 || a->H_v < 1 || a->d < 1 || a->M_max < 1)
+    return TREVS_ERR_INVALID_ARG;
+  if (a->N % a->n_seg) return TREVS_ERR_INVALID_ARG;
+  if (a->k_keep < 1 || a->k_keep > a->N) return TREVS_ERR_INVALID_ARG;
+  if (a->k_div < 0 || a->k_div >= a->k_keep) return TREVS_ERR_INVALID_ARG;
+  const int e = elem_bytes(a->dtype);
+  if (((int64_t)a->d * e) % 16) return TREVS_ERR_INVALID_ARG;
+  if (!finite(a->textual_ratio) || a->textual_ratio < 0.f || a->textual_ratio > 1.f)
+    return TREVS_ERR_INVALID_ARG;
+  if (!finite(a->tau_v) || !finite(a->tau_t) || a->tau_v <= 0.f || a->tau_t <= 0.f)
+    return TREVS_ERR_INVALID_ARG;
+  if (!finite(a->lambda_) || a->lambda_ < 0.f || !finite(a->eps) || a->eps < 0.f)
+    return TREVS_ERR_INVALID_ARG;
+  if (!a->cls_logits || !a->vis_feats || !a->text_emb || !a->kept_idx || !a->kept_feats)
+    return TREVS_ERR_INVALID_ARG;
+  if (!aligned(a->vis_feats, 16) || !aligned(a->text_emb, 16) || !aligned(a->kept_feats, 16) ||
+      !aligned(a->cls_logits, e) || !aligned(a->kept_idx, 4) || !aligned(a->text_len, 4) ||
+      !aligned(a->score_out, 4) || !aligned(a->sal_out, 4) || !aligned(a->rel_out, 4) ||
+      !aligned(a->norm_stats, 4))
+    return TREVS_ERR_INVALID_ARG;
+  if ((int64_t)a->B * a->M_max > INT32_MAX || (int64_t)a->B * a->H_v * a->n_seg > INT32_MAX ||
+      (int64_t)a->B * a->N > INT32_MAX)
+    return TREVS_ERR_UNSUPPORTED;
+  const size_t B = a->B, N = a->N;
+  const Span in[] = {{a->cls_logits, B * a->H_v * N * e},
+                     {a->vis_feats, B * N * a->d * e},
+                     {a->text_emb, B * a->M_max * a->d * e},
+                     {a->text_len, a->text_len ? B * 4 : 0}};
+  const Span out[] = {{a->kept_idx, B * a->k_keep * 4},
+                      {a->kept_feats, B * a->k_keep * a->d * e},
+                      {a->score_out, a->score_out ? B * N * 4 : 0},
+                      {a->sal_out, a->sal_out ? B * N * 4 : 0},
+                      {a->rel_out, a->rel_out ? B * N * 4 : 0},
+                      {a->norm_stats, a->norm_stats ? B * 16 : 0}};
+  if (any_overlap(out, 6, in, 4)) return TREVS_ERR_INVALID_ARG;
+  if (a->k_div > 0) return TREVS_ERR_UNSUPPORTED;
+  if (a->N > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
+  return TREVS_OK;
+}
+
+PrellmLayout prellm_layout(const trevs_prellm_args* a) {
+  PrellmLayout L;
+  size_t off = 0;
+  L.row_stats = off;
+  off = align_up(off + (size_t)a->B * a->H_v * a->n_seg * sizeof(float2));
+  L.inv_tnorm = off;
+  off = align_up(off + (size_t)a->B * a->M_max * sizeof(float));
+  L.sal = off;
+  off = align_up(off + (size_t)a->B * a->N * sizeof(float));
+  L.rel = off;
+  off = align_up(off + (size_t)a->B * a->N * sizeof(float));
+  L.total = off;
+  return L;
+}
+
+// ------------------------------------------------------------------ stage 2
+struct InllmPlan {
+  int n_split, split_len, n_rgroups;
+  size_t part, lse2, head_var, head_sel, score, total;
+};
+
+trevs_status validate_inllm(const trevs_inllm_args* a) {
+  if (!a || a->struct_size != sizeof(trevs_inllm_args)) return TREVS_ERR_INVALID_ARG;
+  if (a->dtype != TREVS_F32 && a->dtype != TREVS_BF16) return TREVS_ERR_INVALID_ARG;
+  if (a->B < 1 || a->S < 1 || a->P < 0 || a->K_in < 1 || a->T_max < 1) return TREVS_ERR_INVALID_ARG;
+  if ((int64_t)a->P + a->K_in + a->T_max > a->S) return TREVS_ERR_INVALID_ARG;
+  if (a->H_q < 1 || a->H_kv < 1 || a->H_q % a->H_kv) return TREVS_ERR_INVALID_ARG;
+  if (a->d_head < 1 || a->D < 1 || a->n_pos < 1) return TREVS_ERR_INVALID_ARG;
+  const int e = elem_bytes(a->dtype);
+  if (((int64_t)a->D * e) % 16 || ((int64_t)a->H_kv * a->d_head * e) % 16) return TREVS_ERR_INVALID_ARG;
+  if (a->n_keep_heads < 1 || a->n_keep_heads > a->H_q) return TREVS_ERR_INVALID_ARG;
+  if (a->k_keep < 1 || a->k_keep > a->K_in) return TREVS_ERR_INVALID_ARG;
+  if (!finite(a->scale) || a->scale <= 0.f) return TREVS_ERR_INVALID_ARG;
+  if (!a->q || !a->k || !a->v || !a->hidden || !a->pos || !a->kept_idx || !a->hidden_out ||
+      !a->k_out || !a->v_out || !a->pos_out)
+    return TREVS_ERR_INVALID_ARG;
+  if (!aligned(a->q, 16) || !aligned(a->k, 16) || !aligned(a->v, 16) || !aligned(a->hidden, 16) ||
+      !aligned(a->hidden_out, 16) || !aligned(a->k_out, 16) || !aligned(a->v_out, 16) ||
+      !aligned(a->pos, 8) || !aligned(a->pos_out, 8) || !aligned(a->text_len, 4) ||
+      !aligned(a->lse_rest, 4) || !aligned(a->kept_idx, 4) || !aligned(a->head_sel, 4) ||
+      !aligned(a->head_var, 4) || !aligned(a->score_out, 4))
+    return TREVS_ERR_INVALID_ARG;
+  if ((int64_t)a->B * a->S > INT32_MAX || (int64_t)a->n_pos * a->B * a->S > INT32_MAX ||
+      (int64_t)a->B * a->H_q * a->T_max > INT32_MAX)
+    return TREVS_ERR_UNSUPPORTED;
+  const size_t B = a->B, S = a->S, So = (size_t)a->S - a->K_in + a->k_keep;
+  const size_t kvrow = (size_t)a->H_kv * a->d_head * e;
+  const Span in[] = {{a->q, B * S * a->H_q * a->d_head * e},
+                     {a->k, B * S * kvrow},
+                     {a->v, B * S * kvrow},
+                     {a->hidden, B * S * a->D * e},
+                     {a->pos, (size_t)a->n_pos * B * S * 8},
+                     {a->text_len, a->text_len ? B * 4 : 0},
+                     {a->lse_rest, a->lse_rest ? B * a->H_q * a->T_max * 4 : 0}};
+  const Span out[] = {{a->kept_idx, B * a->k_keep * 4},
+                      {a->hidden_out, B * So * a->D * e},
+                      {a->k_out, B * So * kvrow},
+                      {a->v_out, B * So * kvrow},
+                      {a->pos_out, (size_t)a->n_pos * B * So * 8},
+                      {a->head_sel, a->head_sel ? B * a->n_keep_heads * 4 : 0},
+                      {a->head_var, a->head_var ? B * a->H_q * 4 : 0},
+                      {a->score_out, a->score_out ? B * a->K_in * 4 : 0}};
+  if (any_overlap(out, 8, in, 7)) return TREVS_ERR_INVALID_ARG;
+  if (a->d_head != 64 && a->d_head != 128 && a->d_head != 256) return TREVS_ERR_UNSUPPORTED;
+  if (a->H_q > 256) return TREVS_ERR_UNSUPPORTED;
+  if (a->K_in > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
+  return TREVS_OK;
+}
+
+// Split of the visual keys for the statistics pass: enough waves to fill the
+// GPU (>= 2048), each split at least 256 keys, split lengths multiples of 32.
+InllmPlan inllm_plan(const trevs_inllm_args* a) {
+  InllmPlan p;
+  const int G = a->H_q / a->H_kv;
+  const int nrb = (G * a->T_max + 31) / 32;
+  const int nw = nrb >= 4 ? 4 : (nrb >= 2 ? 2 : 1);
+  p.n_rgroups = (nrb + nw - 1) / nw;
+  const int64_t base_waves = (int64_t)a->B * a->H_kv * nrb;
+  int n_split = (int)std::min<int64_t>((2048 + base_waves - 1) / base_waves, (a->K_in + 255) / 256);
+  n_split = std::max(n_split, 1);
+  p.split_len = ((a->K_in + n_split - 1) / n_split + 31) / 32 * 32;
+  p.n_split = (a->K_in + p.split_len - 1) / p.split_len;
+  const size_t rows = (size_t)a->B * a->H_q * a->T_max;
+  size_t off = 0;
+  p.part = off;
+  off = align_up(off + rows * p.n_split * sizeof(float4));
+  p.lse2 = off;
+  off = align_up(off + rows * sizeof(float));
+  p.head_var = off;
+  off = align_up(off + (size_t)a->B * a->H_q * sizeof(float));
+  p.head_sel = off;
+  off = align_up(off + (size_t)a->B * a->n_keep_heads * sizeof(int32_t));
+  p.score = off;
+  off = align_up(off + (size_t)a->B * a->K_in * sizeof(float));
+  p.total = off;
+  return p;
+}
+
+trevs_status check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return TREVS_OK;
+  if (!ws || ws_bytes < need || !aligned(ws, kWsAlign)) return TREVS_ERR_WORKSPACE;
+  return TREVS_OK;
+}
+
+int tpr_log2_for(int row_bytes) {
+  const int vpr = row_bytes / 16;
+  const int want = (vpr + 3) / 4;
+  int l = 0;
+  while ((1 << l) < want && l < 8) ++l;
+  return l;
+}
+
+}  // namespace
+
+#define TREVS_TRY(x)                            \
+  do {                                          \
+    const trevs_status st_ = (x);               \
+    if (st_ != TREVS_OK) return st_;            \
+  } while (0)
+#define TREVS_HIP(x)                                   \
+  do {                                                 \
+    if ((x) != hipSuccess) return TREVS_ERR_HIP;       \
+  } while (0)
+
+extern "C" {
+
+size_t trevs_prellm_args_size(void) { return sizeof(trevs_prellm_args); }
+size_t trevs_inllm_args_size(void) { return sizeof(trevs_inllm_args); }
+
+const char* trevs_status_string(trevs_status s) {
+  switch (s) {
+    case TREVS_OK: return "ok";
+    case TREVS_ERR_INVALID_ARG: return "invalid argument";
+    case TREVS_ERR_UNSUPPORTED: return "unsupported by this implementation";
+    case TREVS_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case TREVS_ERR_HIP: return "HIP launch or event error";
+  }
+  return "unknown status";
+}
+
+int32_t trevs_keep_count(float ratio, int32_t n) {
+  if (n < 1) return 0;
+  const double k = floor((double)ratio * n + 0.5);
+  if (!(k >= 1.0)) return 1;
+  return k > n ? n : (int32_t)k;
+}
+
+size_t trevs_prellm_workspace_size(const trevs_prellm_args* a) {
+  const trevs_status st = validate_prellm(a);
+  if (st != TREVS_OK) return 0;
+  return prellm_layout(a).total;
+}
+
+size_t trevs_inllm_workspace_size(const trevs_inllm_args* a) {
+  const trevs_status st = validate_inllm(a);
+  if (st != TREVS_OK) return 0;
+  return inllm_plan(a).total;
+}
+
+size_t trevs_topk_workspace_size(int32_t, int32_t, int32_t) { return 0; }
+
+trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_bytes, void* stream) {
+  TREVS_TRY(validate_prellm(a));
+  const PrellmLayout L = prellm_layout(a);
+  TREVS_TRY(check_ws(ws, ws_bytes, L.total));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = reinterpret_cast<uint8_t*>(ws);
+  const int e = elem_bytes(a->dtype);
+  float2* row_stats = reinterpret_cast<float2*>(w + L.row_stats);
+  float* inv_tnorm = reinterpret_cast<float*>(w + L.inv_tnorm);
+  float* sal = a->sal_out ? a->sal_out : reinterpret_cast<float*>(w + L.sal);
+  float* rel = a->rel_out ? a->rel_out : reinterpret_cast<float*>(w + L.rel);
+
+  PrepArgs pa;
+  pa.cls = a->cls_logits;
+  pa.B = a->B;
+  pa.H = a->H_v;
+  pa.N = a->N;
+  pa.n_seg = a->n_seg;
+  pa.seg_len = a->N / a->n_seg;
+  pa.row_stats = row_stats;
+  pa.text = a->text_emb;
+  pa.text_len = a->text_len;
+  pa.M_max = a->M_max;
+  pa.row_bytes = a->d * e;
+  pa.inv_tnorm = inv_tnorm;
+  pa.n_cls_blocks = a->B * a->H_v * a->n_seg;
+  TREVS_TRY(record(a->events, 0, s));
+  TREVS_HIP(launch_prep(pa, a->dtype, s));
+  TREVS_TRY(record(a->events, 1, s));
+
+  RelArgs ra;
+  ra.cls = a->cls_logits;
+  ra.row_stats = row_stats;
+  ra.H = a->H_v;
+  ra.n_seg = a->n_seg;
+  ra.seg_len = a->N / a->n_seg;
+  ra.Z = a->vis_feats;
+  ra.T = a->text_emb;
+  ra.text_len = a->text_len;
+  ra.inv_tnorm = inv_tnorm;
+  ra.B = a->B;
+  ra.N = a->N;
+  ra.M_max = a->M_max;
+  ra.row_bytes = a->d * e;
+  ra.tiles_per_sample = (a->N + relevance_tile_tokens() - 1) / relevance_tile_tokens();
+  ra.sal = sal;
+  ra.rel = rel;
+  const int MT = a->M_max <= 32 ? 32 : (a->M_max <= 64 ? 64 : 128);
+  TREVS_TRY(record(a->events, 2, s));
+  TREVS_HIP(launch_relevance(ra, a->dtype, MT, s));
+  TREVS_TRY(record(a->events, 3, s));
+
+  SelArgs sa;
+  sa.sal = sal;
+  sa.rel = rel;
+  sa.N = a->N;
+  sa.K = a->k_keep;
+  sa.wv = (float)(2.0 * (1.0 - (double)a->textual_ratio));
+  sa.wt = (float)(2.0 * (double)a->textual_ratio);
+  sa.tau_v = a->tau_v;
+  sa.tau_t = a->tau_t;
+  sa.lam = a->lambda_;
+  sa.eps = a->eps;
+  sa.score_out = a->score_out;
+  sa.norm_stats = a->norm_stats;
+  sa.kept_idx = a->kept_idx;
+  TREVS_TRY(record(a->events, 4, s));
+  TREVS_HIP(launch_prellm_select(sa, a->B, s));
+  TREVS_TRY(record(a->events, 5, s));
+
+  GatherArgs ga;
+  memset(&ga, 0, sizeof(ga));
+  ga.t[0].src = reinterpret_cast<const uint8_t*>(a->vis_feats);
+  ga.t[0].dst = reinterpret_cast<uint8_t*>(a->kept_feats);
+  ga.t[0].row_bytes = a->d * e;
+  ga.t[0].src_bstride = (long long)a->N * a->d * e;
+  ga.t[0].dst_bstride = (long long)a->k_keep * a->d * e;
+  ga.t[0].tpr_log2 = tpr_log2_for(a->d * e);
+  ga.n_tensors = 1;
+  ga.idx = a->kept_idx;
+  ga.B = a->B;
+  ga.rows_out = a->k_keep;
+  ga.P = 0;
+  ga.K_in = a->N;
+  ga.n_kept = a->k_keep;
+  TREVS_TRY(record(a->events, 6, s));
+  TREVS_HIP(launch_gather(ga, s));
+  TREVS_TRY(record(a->events, 7, s));
+  return TREVS_OK;
+}
+
+trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_bytes, void* stream) {
+  TREVS_TRY(validate_inllm(a));
+  const InllmPlan p = inllm_plan(a);
+  TREVS_TRY(check_ws(ws, ws_bytes, p.total));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = reinterpret_cast<uint8_t*>(ws);
+  const int e = elem_bytes(a->dtype);
+  const int G = a->H_q / a->H_kv;
+  const float scale_log2e = a->scale * kLog2e;
+  float4* part = reinterpret_cast<float4*>(w + p.part);
+  float* lse2 = reinterpret_cast<float*>(w + p.lse2);
+  float* head_var = a->head_var ? a->head_var : reinterpret_cast<float*>(w + p.head_var);
+  int32_t* head_sel = a->head_sel ? a->head_sel : reinterpret_cast<int32_t*>(w + p.head_sel);
+  float* score = a->score_out ? a->score_out : reinterpret_cast<float*>(w + p.score);
+
+  StatsArgs ta;
+  ta.q = a->q;
+  ta.k = a->k;
+  ta.B = a->B;
+  ta.S = a->S;
+  ta.P = a->P;
+  ta.K_in = a->K_in;
+  ta.T_max = a->T_max;
+  ta.H_q = a->H_q;
+  ta.H_kv = a->H_kv;
+  ta.G = G;
+  ta.scale_log2e = scale_log2e;
+  ta.n_split = p.n_split;
+  ta.split_len = p.split_len;
+  ta.n_rgroups = p.n_rgroups;
+  ta.part = part;
+  TREVS_TRY(record(a->events, 0, s));
+  TREVS_HIP(launch_stats(ta, a->dtype, a->d_head, s));
+  TREVS_TRY(record(a->events, 1, s));
+
+  HeadArgs ha;
+  ha.part = part;
+  ha.B = a->B;
+  ha.H_q = a->H_q;
+  ha.T_max = a->T_max;
+  ha.K_in = a->K_in;
+  ha.n_split = p.n_split;
+  ha.n_keep = a->n_keep_heads;
+  ha.text_len = a->text_len;
+  ha.lse_rest = a->lse_rest;
+  ha.lse2 = lse2;
+  ha.head_var = head_var;
+  ha.head_sel = head_sel;
+  TREVS_TRY(record(a->events, 2, s));
+  TREVS_HIP(launch_heads(ha, s));
+  TREVS_TRY(record(a->events, 3, s));
+
+  ScoreArgs sa;
+  sa.q = a->q;
+  sa.k = a->k;
+  sa.B = a->B;
+  sa.S = a->S;
+  sa.P = a->P;
+  sa.K_in = a->K_in;
+  sa.T_max = a->T_max;
+  sa.H_q = a->H_q;
+  sa.H_kv = a->H_kv;
+  sa.G = G;
+  sa.n_keep = a->n_keep_heads;
+  sa.scale_log2e = scale_log2e;
+  sa.lse2 = lse2;
+  sa.head_sel = head_sel;
+  sa.text_len = a->text_len;
+  sa.p = score;
+  TREVS_TRY(record(a->events, 4, s));
+  TREVS_HIP(launch_score(sa, a->dtype, a->d_head, s));
+  TREVS_TRY(record(a->events, 5, s));
+
+  TREVS_TRY(record(a->events, 6, s));
+  TREVS_HIP(launch_topk(score, a->B, a->K_in, a->k_keep, a->kept_idx, s));
+  TREVS_TRY(record(a->events, 7, s));
+
+  const int So = a->S - a->K_in + a->k_keep;
+  const int kvrow = a->H_kv * a->d_head * e;
+  GatherArgs ga;
+  memset(&ga, 0, sizeof(ga));
+  const void* srcs[3] = {a->hidden, a->k, a->v};
+  void* dsts[3] = {a->hidden_out, a->k_out, a->v_out};
+  const int rowb[3] = {a->D * e, kvrow, kvrow};
+  for (int t = 0; t < 3; ++t) {
+    ga.t[t].src = reinterpret_cast<const uint8_t*>(srcs[t]);
+    ga.t[t].dst = reinterpret_cast<uint8_t*>(dsts[t]);
+    ga.t[t].row_bytes = rowb[t];
+    ga.t[t].src_bstride = (long long)a->S * rowb[t];
+    ga.t[t].dst_bstride = (long long)So * rowb[t];
+    ga.t[t].tpr_log2 = tpr_log2_for(rowb[t]);
+  }
+  ga.n_tensors = 3;
+  ga.idx = a->kept_idx;
+  ga.B = a->B;
+  ga.rows_out = So;
+  ga.P = a->P;
+  ga.K_in = a->K_in;
+  ga.n_kept = a->k_keep;
+  ga.pos = a->pos;
+  ga.pos_out = a->pos_out;
+  ga.n_pos = a->n_pos;
+  ga.S = a->S;
+  TREVS_TRY(record(a->events, 8, s));
+  TREVS_HIP(launch_gather(ga, s));
+  TREVS_TRY(record(a->events, 9, s));
+  return TREVS_OK;
+}
+
+trevs_status trevs_topk_select(const float* scores, int32_t B, int32_t N, int32_t K, int32_t* kept_idx,
+                               void* ws, size_t ws_bytes, void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!scores || !kept_idx || B < 1 || N < 1 || K < 1 || K > N) return TREVS_ERR_INVALID_ARG;
+  if (!aligned(scores, 4) || !aligned(kept_idx, 4)) return TREVS_ERR_INVALID_ARG;
+  if (overlap(Span{scores, (size_t)B * N * 4}, Span{kept_idx, (size_t)B * K * 4}))
+    return TREVS_ERR_INVALID_ARG;
+  if (N > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
+  TREVS_HIP(launch_topk(scores, B, N, K, kept_idx, reinterpret_cast<hipStream_t>(stream)));
+  return TREVS_OK;
+}
+
+}  // extern "C"

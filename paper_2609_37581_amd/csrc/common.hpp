@@ -1,0 +1,145 @@
+// Device primitives shared by the TReVS kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace trevs {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Input element tags.  Every operand fragment a lane holds is 64 bytes: 32
+// bf16 values or 16 fp32 values.
+struct BF16 {
+  static constexpr int kBytes = 2;
+};
+struct F32 {
+  static constexpr int kBytes = 4;
+};
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float load_scalar(const void* p, size_t i, BF16) {
+  return __uint_as_float(uint32_t(reinterpret_cast<const uint16_t*>(p)[i]) << 16);
+}
+__device__ __forceinline__ float load_scalar(const void* p, size_t i, F32) {
+  return reinterpret_cast<const float*>(p)[i];
+}
+
+// Sum of squares of the values packed in a 16-byte vector.
+__device__ __forceinline__ float sumsq(u32x4 v, BF16) {
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float lo = bf16_lo(v[j]), hi = bf16_hi(v[j]);
+    s = fmaf(lo, lo, s);
+    s = fmaf(hi, hi, s);
+  }
+  return s;
+}
+__device__ __forceinline__ float sumsq(u32x4 v, F32) {
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float x = __uint_as_float(v[j]);
+    s = fmaf(x, x, s);
+  }
+  return s;
+}
+
+// C[32x32] += A[32 x k] * B[k x 32] over one 64-byte fragment per lane.
+// Lane l supplies row (l % 32) of A and column (l % 32) of B; its half
+// (l / 32) selects which 64-byte half of a 128-byte row chunk it carries.
+// A and B lanes carry the same k values element for element, so any
+// assignment of k to (half, element) that both operands share contracts
+// correctly.  Output layout: lane l holds column (l % 32), register r holds
+// row 8*(r/4) + 4*(l/32) + (r%4).
+__device__ __forceinline__ f32x16 mfma_frag(const u32x4 (&a)[4], const u32x4 (&b)[4], f32x16 c,
+                                            BF16) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[s]),
+                                                __builtin_bit_cast(bf16x8, b[s]), c, 0, 0, 0);
+  return c;
+}
+__device__ __forceinline__ f32x16 mfma_frag(const u32x4 (&a)[4], const u32x4 (&b)[4], f32x16 c,
+                                            F32) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[s][j]), __uint_as_float(b[s][j]),
+                                               c, 0, 0, 0);
+  return c;
+}
+
+// Row of the 32x32 output block held by register r of a lane in half `half`.
+__device__ __forceinline__ int mfma_row(int r, int half) { return 8 * (r >> 2) + 4 * half + (r & 3); }
+
+__device__ __forceinline__ u32x4 ldg16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ u32x4 ldg16_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ void stg16_stream(void* p, u32x4 v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
+__device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
+
+// ---------------------------------------------------------------- reductions
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, o, kWave));
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
+  return v;
+}
+// Inclusive prefix sum across the wave.
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int t = __shfl_up(v, o, kWave);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+// Order-preserving map from fp32 to uint32 (-0 taken as +0).
+__device__ __forceinline__ uint32_t f2key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key2f(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// Workgroup-id remap so that consecutive logical tiles land on the same XCD:
+// the hardware hands workgroup w to XCD (w % 8); XCD x gets the contiguous
+// logical range starting at x*(W/8) + min(x, W%8).
+__device__ __forceinline__ int xcd_remap(int w, int W) {
+  const int per = W >> 3, rem = W & 7, x = w & 7, local = w >> 3;
+  return x * per + min(x, rem) + local;
+}
+
+}  // namespace trevs

@@ -1,0 +1,110 @@
+// Internal kernel argument blocks and launchers (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace trevs {
+
+// ---------------------------------------------------------------- stage 1
+struct PrepArgs {
+  const void* cls;           // [B,H,N]
+  int B, H, N, n_seg, seg_len;
+  float2* row_stats;         // [B*H*n_seg]: (row max * log2 e, 1 / sum of exp)
+  const void* text;          // [B,M_max,d]
+  const int32_t* text_len;   // [B] or null
+  int M_max, row_bytes;      // row_bytes = d * elem
+  float* inv_tnorm;          // [B*M_max]: 1/max(||t_j||, 1e-12), 0 for j >= M_b
+  int n_cls_blocks;          // blocks [0, n_cls_blocks) do [CLS] rows, the rest text rows
+};
+
+struct RelArgs {
+  const void* cls;
+  const float2* row_stats;
+  int H, n_seg, seg_len;
+  const void* Z;             // [B,N,d]
+  const void* T;             // [B,M_max,d]
+  const int32_t* text_len;
+  const float* inv_tnorm;
+  int B, N, M_max, row_bytes, tiles_per_sample;
+  float* sal;                // [B,N]
+  float* rel;                // [B,N]
+};
+
+struct SelArgs {
+  const float* sal;
+  const float* rel;
+  int N, K;
+  float wv, wt, tau_v, tau_t, lam, eps;
+  float* score_out;          // [B,N] or null
+  float* norm_stats;         // [B,4] or null
+  int32_t* kept_idx;         // [B,K]
+};
+
+// ---------------------------------------------------------------- stage 2
+struct StatsArgs {
+  const void* q;             // [B,S,H_q,dh]
+  const void* k;             // [B,S,H_kv,dh]
+  int B, S, P, K_in, T_max, H_q, H_kv, G;
+  float scale_log2e;         // scale * log2 e
+  int n_split, split_len;    // visual columns per split (multiple of 32)
+  int n_rgroups;             // workgroups along the (head-in-group, text row) axis
+  float4* part;              // [B,H_q,T_max,n_split]: (max, sum e, sum e^2, -) in log2 units
+};
+
+struct HeadArgs {
+  const float4* part;
+  int B, H_q, T_max, K_in, n_split, n_keep;
+  const int32_t* text_len;
+  const float* lse_rest;     // [B,H_q,T_max] natural log, or null
+  float* lse2;               // [B,H_q,T_max] row log-sum-exp in log2 units
+  float* head_var;           // [B,H_q]
+  int32_t* head_sel;         // [B,n_keep]
+};
+
+struct ScoreArgs {
+  const void* q;
+  const void* k;
+  int B, S, P, K_in, T_max, H_q, H_kv, G, n_keep;
+  float scale_log2e;
+  const float* lse2;
+  const int32_t* head_sel;
+  const int32_t* text_len;
+  float* p;                  // [B,K_in]
+};
+
+// ---------------------------------------------------------------- gather
+constexpr int kGatherMaxTensors = 4;
+struct GatherTensor {
+  const uint8_t* src;
+  uint8_t* dst;
+  long long src_bstride, dst_bstride;  // bytes per sample
+  int row_bytes;                       // multiple of 16
+  int tpr_log2;                        // log2(threads per row), threads per row <= 256
+};
+struct GatherArgs {
+  GatherTensor t[kGatherMaxTensors];
+  int n_tensors;
+  const int32_t* idx;        // [B,n_kept] kept rows relative to the selected block
+  int B, rows_out, P, K_in, n_kept;
+  const int64_t* pos;        // [n_pos,B,S] or null
+  int64_t* pos_out;          // [n_pos,B,rows_out]
+  int n_pos, S;
+};
+constexpr int kGatherRowsPerBlock = 16;
+constexpr int kGatherThreads = 256;
+
+hipError_t launch_prep(const PrepArgs& a, int dtype, hipStream_t s);
+hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s);
+int relevance_tile_tokens();
+hipError_t launch_prellm_select(const SelArgs& a, int B, hipStream_t s);
+hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, hipStream_t s);
+hipError_t launch_stats(const StatsArgs& a, int dtype, int dh, hipStream_t s);
+hipError_t launch_heads(const HeadArgs& a, hipStream_t s);
+hipError_t launch_score(const ScoreArgs& a, int dtype, int dh, hipStream_t s);
+hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
+
+// Number of 32-row text blocks the token-score kernel handles per workgroup.
+int score_qblocks(int T_max);
+
+}  // namespace trevs

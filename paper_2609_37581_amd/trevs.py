@@ -1,0 +1,334 @@
+"""ctypes binding of libtrevs.so (include/trevs.h).
+
+Argument marshalling only: every step of both pruning stages runs in the HIP
+kernels of the library.  PyTorch supplies device memory (outputs, workspace)
+and the current stream.  If the library is missing the import of any entry
+point raises; there is no fallback path.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtrevs.so")
+
+TREVS_F32, TREVS_BF16 = 0, 1
+PRELLM_NUM_KERNELS = 4
+INLLM_NUM_KERNELS = 5
+MAX_SELECT_N = 32768
+PRELLM_KERNELS = ("prep", "relevance", "select", "gather")
+INLLM_KERNELS = ("t2v_stats", "head_select", "token_score", "topk", "compaction")
+
+_STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "workspace", 4: "hip error"}
+
+
+class TrevsError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {_STATUS.get(status, status)} (status {status})")
+
+
+c_int32, c_uint32, c_float, c_void_p, c_size_t = (ctypes.c_int32, ctypes.c_uint32, ctypes.c_float,
+                                                   ctypes.c_void_p, ctypes.c_size_t)
+
+
+class PrellmArgs(ctypes.Structure):
+    _fields_ = [("struct_size", c_uint32), ("B", c_int32), ("N", c_int32), ("n_seg", c_int32),
+                ("H_v", c_int32), ("d", c_int32), ("M_max", c_int32), ("k_keep", c_int32),
+                ("k_div", c_int32), ("textual_ratio", c_float), ("tau_v", c_float),
+                ("tau_t", c_float), ("lambda_", c_float), ("eps", c_float), ("dtype", c_int32),
+                ("cls_logits", c_void_p), ("vis_feats", c_void_p), ("text_emb", c_void_p),
+                ("text_len", c_void_p), ("kept_idx", c_void_p), ("kept_feats", c_void_p),
+                ("score_out", c_void_p), ("sal_out", c_void_p), ("rel_out", c_void_p),
+                ("norm_stats", c_void_p), ("events", c_void_p)]
+
+
+class InllmArgs(ctypes.Structure):
+    _fields_ = [("struct_size", c_uint32), ("B", c_int32), ("S", c_int32), ("P", c_int32),
+                ("K_in", c_int32), ("T_max", c_int32), ("H_q", c_int32), ("H_kv", c_int32),
+                ("d_head", c_int32), ("D", c_int32), ("n_pos", c_int32),
+                ("n_keep_heads", c_int32), ("k_keep", c_int32), ("scale", c_float),
+                ("dtype", c_int32), ("q", c_void_p), ("k", c_void_p), ("v", c_void_p),
+                ("hidden", c_void_p), ("pos", c_void_p), ("text_len", c_void_p),
+                ("lse_rest", c_void_p), ("kept_idx", c_void_p), ("hidden_out", c_void_p),
+                ("k_out", c_void_p), ("v_out", c_void_p), ("pos_out", c_void_p),
+                ("head_sel", c_void_p), ("head_var", c_void_p), ("score_out", c_void_p),
+                ("events", c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_37581_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.trevs_prellm_workspace_size.argtypes = [ctypes.POINTER(PrellmArgs)]
+        L.trevs_prellm_workspace_size.restype = c_size_t
+        L.trevs_inllm_workspace_size.argtypes = [ctypes.POINTER(InllmArgs)]
+        L.trevs_inllm_workspace_size.restype = c_size_t
+        L.trevs_topk_workspace_size.argtypes = [c_int32, c_int32, c_int32]
+        L.trevs_topk_workspace_size.restype = c_size_t
+        L.trevs_prellm_prune.argtypes = [ctypes.POINTER(PrellmArgs), c_void_p, c_size_t, c_void_p]
+        L.trevs_prellm_prune.restype = ctypes.c_int
+        L.trevs_inllm_prune.argtypes = [ctypes.POINTER(InllmArgs), c_void_p, c_size_t, c_void_p]
+        L.trevs_inllm_prune.restype = ctypes.c_int
+        L.trevs_topk_select.argtypes = [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                        c_size_t, c_void_p]
+        L.trevs_topk_select.restype = ctypes.c_int
+        L.trevs_status_string.argtypes = [ctypes.c_int]
+        L.trevs_status_string.restype = ctypes.c_char_p
+        L.trevs_keep_count.argtypes = [c_float, c_int32]
+        L.trevs_keep_count.restype = c_int32
+        L.trevs_prellm_args_size.restype = c_size_t
+        L.trevs_inllm_args_size.restype = c_size_t
+        if (L.trevs_prellm_args_size() != ctypes.sizeof(PrellmArgs)
+                or L.trevs_inllm_args_size() != ctypes.sizeof(InllmArgs)):
+            raise RuntimeError("libtrevs.so argument structs do not match this binding")
+        _lib = L
+    return _lib
+
+
+def keep_count(ratio, n):
+    return int(lib().trevs_keep_count(ratio, n))
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return TREVS_F32
+    if t.dtype == torch.bfloat16:
+        return TREVS_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _check(t, name, device, ndim=None, dtype=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class _EventArray:
+    def __init__(self, events, n_kernels):
+        if events is None:
+            self.ptr = None
+            return
+        if len(events) != 2 * n_kernels:
+            raise ValueError(f"events must hold {2 * n_kernels} handles (None allowed)")
+        self.arr = (c_void_p * len(events))(*[e for e in events])
+        self.ptr = ctypes.cast(self.arr, c_void_p)
+
+
+class Prellm:
+    """Stage 1 with outputs and workspace allocated once; call() enqueues it."""
+
+    def __init__(self, cls_logits, vis_feats, text_emb, text_len=None, *, k_keep, n_seg=1,
+                 k_div=0, textual_ratio=0.5, tau_v=1.4, tau_t=1.0, lambda_=1.0, eps=1e-8,
+                 want_scores=False):
+        dev = vis_feats.device
+        _check(vis_feats, "vis_feats", dev, 3)
+        dt = vis_feats.dtype
+        _check(cls_logits, "cls_logits", dev, 3, dt)
+        _check(text_emb, "text_emb", dev, 3, dt)
+        if text_len is not None:
+            _check(text_len, "text_len", dev, 1, torch.int32)
+        B, N, d = vis_feats.shape
+        H_v = cls_logits.shape[1]
+        M_max = text_emb.shape[1]
+        if cls_logits.shape != (B, H_v, N) or text_emb.shape != (B, M_max, d):
+            raise ValueError("inconsistent stage-1 shapes")
+        if text_len is not None and text_len.shape != (B,):
+            raise ValueError("text_len must be [B]")
+        self.inputs = (cls_logits, vis_feats, text_emb, text_len)
+        self.kept_idx = torch.empty((B, k_keep), dtype=torch.int32, device=dev)
+        self.kept_feats = torch.empty((B, k_keep, d), dtype=dt, device=dev)
+        if want_scores:
+            self.score = torch.empty((B, N), dtype=torch.float32, device=dev)
+            self.sal = torch.empty((B, N), dtype=torch.float32, device=dev)
+            self.rel = torch.empty((B, N), dtype=torch.float32, device=dev)
+            self.norm_stats = torch.empty((B, 4), dtype=torch.float32, device=dev)
+        else:
+            self.score = self.sal = self.rel = self.norm_stats = None
+        a = PrellmArgs()
+        a.struct_size = ctypes.sizeof(PrellmArgs)
+        a.B, a.N, a.n_seg, a.H_v, a.d, a.M_max = B, N, n_seg, H_v, d, M_max
+        a.k_keep, a.k_div = k_keep, k_div
+        a.textual_ratio, a.tau_v, a.tau_t, a.lambda_, a.eps = textual_ratio, tau_v, tau_t, lambda_, eps
+        a.dtype = _dtype_code(vis_feats)
+        a.cls_logits, a.vis_feats, a.text_emb = _ptr(cls_logits), _ptr(vis_feats), _ptr(text_emb)
+        a.text_len = _ptr(text_len)
+        a.kept_idx, a.kept_feats = _ptr(self.kept_idx), _ptr(self.kept_feats)
+        a.score_out, a.sal_out, a.rel_out = _ptr(self.score), _ptr(self.sal), _ptr(self.rel)
+        a.norm_stats = _ptr(self.norm_stats)
+        self.args = a
+        ws = lib().trevs_prellm_workspace_size(ctypes.byref(a))
+        if ws == 0:
+            # invalid arguments: let the call report the precise status
+            st = lib().trevs_prellm_prune(ctypes.byref(a), None, 0, None)
+            raise TrevsError(st, "trevs_prellm_prune")
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
+
+    def __call__(self, stream=None, events=None):
+        ev = _EventArray(events, PRELLM_NUM_KERNELS)
+        self.args.events = ev.ptr
+        st = lib().trevs_prellm_prune(ctypes.byref(self.args), self.workspace.data_ptr(),
+                                      self.workspace.numel(), _stream(stream))
+        self.args.events = None
+        if st:
+            raise TrevsError(st, "trevs_prellm_prune")
+        return self.kept_idx, self.kept_feats
+
+
+def prellm_prune(cls_logits, vis_feats, text_emb, text_len=None, **kw):
+    """Stage 1 (Sec. 4.1): returns (kept_idx [B,K1] int32, kept_feats [B,K1,d]),
+    plus a dict of scores when want_scores=True."""
+    call = Prellm(cls_logits, vis_feats, text_emb, text_len, **kw)
+    idx, feats = call()
+    if kw.get("want_scores"):
+        return idx, feats, dict(score=call.score, sal=call.sal, rel=call.rel,
+                                norm_stats=call.norm_stats)
+    return idx, feats
+
+
+class Inllm:
+    """Stage 2 with outputs and workspace allocated once; call() enqueues it."""
+
+    def __init__(self, q, k, v, hidden, pos, text_len=None, *, P, K_in, n_keep_heads, k_keep,
+                 scale=None, lse_rest=None, want_scores=False):
+        dev = hidden.device
+        _check(hidden, "hidden", dev, 3)
+        dt = hidden.dtype
+        _check(q, "q", dev, 4, dt)
+        _check(k, "k", dev, 4, dt)
+        _check(v, "v", dev, 4, dt)
+        _check(pos, "pos", dev, 3, torch.int64)
+        if text_len is not None:
+            _check(text_len, "text_len", dev, 1, torch.int32)
+        if lse_rest is not None:
+            _check(lse_rest, "lse_rest", dev, 3, torch.float32)
+        B, S, D = hidden.shape
+        H_q, d_head = q.shape[2], q.shape[3]
+        H_kv = k.shape[2]
+        n_pos = pos.shape[0]
+        T_max = S - P - K_in
+        if q.shape[:2] != (B, S) or k.shape != (B, S, H_kv, d_head) or v.shape != k.shape:
+            raise ValueError("inconsistent stage-2 shapes")
+        if pos.shape != (n_pos, B, S):
+            raise ValueError("pos must be [n_pos,B,S]")
+        if T_max < 1:
+            raise ValueError("no text rows after the visual block")
+        if lse_rest is not None and lse_rest.shape != (B, H_q, T_max):
+            raise ValueError("lse_rest must be [B,H_q,T_max]")
+        So = S - K_in + k_keep
+        self.inputs = (q, k, v, hidden, pos, text_len, lse_rest)
+        self.kept_idx = torch.empty((B, k_keep), dtype=torch.int32, device=dev)
+        self.hidden_out = torch.empty((B, So, D), dtype=dt, device=dev)
+        self.k_out = torch.empty((B, So, H_kv, d_head), dtype=dt, device=dev)
+        self.v_out = torch.empty((B, So, H_kv, d_head), dtype=dt, device=dev)
+        self.pos_out = torch.empty((n_pos, B, So), dtype=torch.int64, device=dev)
+        if want_scores:
+            self.head_sel = torch.empty((B, n_keep_heads), dtype=torch.int32, device=dev)
+            self.head_var = torch.empty((B, H_q), dtype=torch.float32, device=dev)
+            self.score = torch.empty((B, K_in), dtype=torch.float32, device=dev)
+        else:
+            self.head_sel = self.head_var = self.score = None
+        a = InllmArgs()
+        a.struct_size = ctypes.sizeof(InllmArgs)
+        a.B, a.S, a.P, a.K_in, a.T_max = B, S, P, K_in, T_max
+        a.H_q, a.H_kv, a.d_head, a.D, a.n_pos = H_q, H_kv, d_head, D, n_pos
+        a.n_keep_heads, a.k_keep = n_keep_heads, k_keep
+        a.scale = float(scale) if scale is not None else d_head ** -0.5
+        a.dtype = _dtype_code(hidden)
+        a.q, a.k, a.v, a.hidden, a.pos = _ptr(q), _ptr(k), _ptr(v), _ptr(hidden), _ptr(pos)
+        a.text_len, a.lse_rest = _ptr(text_len), _ptr(lse_rest)
+        a.kept_idx, a.hidden_out = _ptr(self.kept_idx), _ptr(self.hidden_out)
+        a.k_out, a.v_out, a.pos_out = _ptr(self.k_out), _ptr(self.v_out), _ptr(self.pos_out)
+        a.head_sel, a.head_var, a.score_out = _ptr(self.head_sel), _ptr(self.head_var), _ptr(self.score)
+        self.args = a
+        ws = lib().trevs_inllm_workspace_size(ctypes.byref(a))
+        if ws == 0:
+            st = lib().trevs_inllm_prune(ctypes.byref(a), None, 0, None)
+            raise TrevsError(st, "trevs_inllm_prune")
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
+
+    def __call__(self, stream=None, events=None):
+        ev = _EventArray(events, INLLM_NUM_KERNELS)
+        self.args.events = ev.ptr
+        st = lib().trevs_inllm_prune(ctypes.byref(self.args), self.workspace.data_ptr(),
+                                     self.workspace.numel(), _stream(stream))
+        self.args.events = None
+        if st:
+            raise TrevsError(st, "trevs_inllm_prune")
+        return self.kept_idx, self.hidden_out, self.k_out, self.v_out, self.pos_out
+
+
+def inllm_prune(q, k, v, hidden, pos, text_len=None, **kw):
+    """Stage 2 (Sec. 4.2): returns (kept_idx, hidden_out, k_out, v_out,
+    pos_out), plus a dict of head_sel/head_var/score when want_scores=True."""
+    call = Inllm(q, k, v, hidden, pos, text_len, **kw)
+    out = call()
+    if kw.get("want_scores"):
+        return out + (dict(head_sel=call.head_sel, head_var=call.head_var, score=call.score),)
+    return out
+
+
+def topk_select(scores, k, stream=None):
+    """Stable top-k of each row of scores [B,N] (fp32, device) -> int32 [B,k]
+    ascending."""
+    _check(scores, "scores", scores.device, 2, torch.float32)
+    B, N = scores.shape
+    out = torch.empty((B, k), dtype=torch.int32, device=scores.device)
+    st = lib().trevs_topk_select(scores.data_ptr(), B, N, k, out.data_ptr(), None, 0, _stream(stream))
+    if st:
+        raise TrevsError(st, "trevs_topk_select")
+    return out
+
+
+# ---------------------------------------------------------------- HIP events
+class HipEvents:
+    """A pool of hipEvent_t handles created through the HIP runtime that torch
+    has already loaded, for the per-kernel event slots of the entry points."""
+
+    def __init__(self, n):
+        self.rt = ctypes.CDLL("libamdhip64.so")
+        self.rt.hipEventCreate.argtypes = [ctypes.POINTER(c_void_p)]
+        self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), c_void_p, c_void_p]
+        self.rt.hipEventDestroy.argtypes = [c_void_p]
+        self.handles = []
+        for _ in range(n):
+            h = c_void_p()
+            if self.rt.hipEventCreate(ctypes.byref(h)):
+                raise RuntimeError("hipEventCreate failed")
+            self.handles.append(h.value)
+
+    def elapsed_ms(self, i, j):
+        ms = ctypes.c_float()
+        if self.rt.hipEventElapsedTime(ctypes.byref(ms), self.handles[i], self.handles[j]):
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def close(self):
+        for h in self.handles:
+            self.rt.hipEventDestroy(h)
+        self.handles = []

@@ -130,14 +130,17 @@ def sweep():
 
 
 def to_storage(x, dtype):
-    """float64 -> float32, or -> bfloat16 bit patterns (uint16) by rounding the
-    float32 value to nearest even."""
+    """float64/float32 -> float32, or -> bfloat16 bit patterns (uint16) by
+    rounding the float32 value to nearest even."""
     f = np.ascontiguousarray(x, dtype=np.float32)
     if dtype == "f32":
         return f
-    u = f.view(np.uint32).astype(np.uint64)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return r.astype(np.uint16)
+    u = f.view(np.uint32).copy()
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    u += np.uint32(0x7FFF)
+    u += lsb
+    u >>= np.uint32(16)
+    return u.astype(np.uint16)
 
 
 def _rng(w, stage, b):
@@ -189,7 +192,7 @@ def stage1_inputs(w):
         sal = np.sort(rng.choice(rest, size=w.n_sal, replace=False))
         L = rng.standard_normal((H, N))
         L[:, sal] += 4.0
-        Z = rng.standard_normal((N, d)) / math.sqrt(d)
+        Z = rng.standard_normal((N, d), dtype=np.float32) * np.float32(1 / math.sqrt(d))
         T = rng.standard_normal((int(lens[b]), d)) / math.sqrt(d)
         u = T.mean(axis=0)
         u /= np.linalg.norm(u)
@@ -197,7 +200,7 @@ def stage1_inputs(w):
             g = rng.standard_normal(d)
             g -= (g @ u) * u
             g /= np.linalg.norm(g)
-            Z[i] = np.linalg.norm(Z[i]) * (0.6 * u + 0.8 * g)
+            Z[i] = np.linalg.norm(Z[i].astype(np.float64)) * (0.6 * u + 0.8 * g)
         if w.tie_stress:
             # a quarter of the tokens copy the logits column and feature row
             # of one of 64 prototype tokens
@@ -257,19 +260,19 @@ def stage2_inputs(w, with_lse_rest=False):
     for b in range(B):
         rng = _rng(w, 2, b)
         beta = rng.permutation(np.linspace(0.5, 2.0, Hq))
-        Q = rng.standard_normal((S, Hq, dh)) * beta[None, :, None]
-        Kt = rng.standard_normal((S, Hkv, dh))
-        Vt = rng.standard_normal((S, Hkv, dh))
-        Hd = rng.standard_normal((S, D))
+        Q = rng.standard_normal((S, Hq, dh), dtype=np.float32) * beta[None, :, None].astype(np.float32)
+        Kt = rng.standard_normal((S, Hkv, dh), dtype=np.float32)
+        Vt = rng.standard_normal((S, Hkv, dh), dtype=np.float32)
+        Hd = rng.standard_normal((S, D), dtype=np.float32)
         sens = np.sort(rng.choice(Hq, size=max(1, Hq // 4), replace=False))
         n_rel = max(1, w.K2 // 2)
         rel = np.sort(rng.choice(w.K1, size=n_rel, replace=False))
         c = rng.standard_normal((Hkv, dh))
         c /= np.linalg.norm(c, axis=1, keepdims=True)
         for g in range(Hkv):
-            Kt[w.P + rel, g, :] += a * c[g]
+            Kt[w.P + rel, g, :] += (a * c[g]).astype(np.float32)
         for h in sens:
-            Q[w.P + w.K1:, h, :] += a * c[h // G]
+            Q[w.P + w.K1:, h, :] += (a * c[h // G]).astype(np.float32)
         kept_vis = np.sort(rng.choice(w.N, size=w.K1, replace=False))
         q[b] = to_storage(Q, w.dtype)
         k[b] = to_storage(Kt, w.dtype)

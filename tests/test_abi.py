@@ -1,0 +1,134 @@
+"""The C ABI without a GPU: the library loads, exports every function the
+header declares, mirrors the argument structs, and rejects invalid arguments
+on the host before any HIP call."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_37581_amd import trevs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "trevs.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(trevs_\w+)\s*\(", text)))
+
+
+def test_header_compiles_as_c99():
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-x", "c", HEADER],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+def test_every_declared_symbol_is_exported():
+    L = trevs.lib()
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(L, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", trevs.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    exported = set(re.findall(r" T (trevs_\w+)", out))
+    assert set(names) <= exported
+
+
+def test_struct_mirror_sizes():
+    L = trevs.lib()
+    assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 152
+    assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 192
+
+
+def test_status_strings_and_keep_count():
+    L = trevs.lib()
+    for s in range(5):
+        assert L.trevs_status_string(s)
+    assert [trevs.keep_count(r, 576) for r in (0.5, 0.25, 1 / 9, 1 / 18)] == [288, 144, 64, 32]
+    assert trevs.keep_count(0.0, 10) == 1 and trevs.keep_count(2.0, 10) == 10
+    assert trevs.keep_count(0.5, 0) == 0
+
+
+def _prellm(**kw):
+    a = trevs.PrellmArgs()
+    a.struct_size = ctypes.sizeof(a)
+    a.B, a.N, a.n_seg, a.H_v, a.d, a.M_max, a.k_keep = 2, 576, 1, 16, 4096, 32, 192
+    a.textual_ratio, a.tau_v, a.tau_t, a.lambda_, a.eps = 0.5, 1.4, 1.0, 1.0, 1e-8
+    a.dtype = trevs.TREVS_BF16
+    base = 1 << 40
+    a.cls_logits, a.vis_feats, a.text_emb = base, base + (1 << 32), base + (2 << 32)
+    a.kept_idx, a.kept_feats = base + (3 << 32), base + (4 << 32)
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def _inllm(**kw):
+    a = trevs.InllmArgs()
+    a.struct_size = ctypes.sizeof(a)
+    a.B, a.S, a.P, a.K_in, a.T_max = 2, 259, 35, 192, 32
+    a.H_q, a.H_kv, a.d_head, a.D, a.n_pos = 32, 32, 128, 4096, 1
+    a.n_keep_heads, a.k_keep, a.scale, a.dtype = 16, 64, 128 ** -0.5, trevs.TREVS_BF16
+    base = 1 << 40
+    for i, name in enumerate(["q", "k", "v", "hidden", "pos", "kept_idx", "hidden_out", "k_out",
+                              "v_out", "pos_out"]):
+        setattr(a, name, base + (i << 32))
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def test_workspace_size_is_positive_for_valid_args():
+    L = trevs.lib()
+    assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm())) > 0
+    assert L.trevs_inllm_workspace_size(ctypes.byref(_inllm())) > 0
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(k_keep=0), 1), (dict(k_keep=577), 1), (dict(n_seg=5), 1), (dict(d=4095), 1),
+    (dict(textual_ratio=-0.1), 1), (dict(textual_ratio=float("nan")), 1), (dict(tau_v=0.0), 1),
+    (dict(eps=-1.0), 1), (dict(dtype=7), 1), (dict(vis_feats=None), 1),
+    (dict(kept_feats=(1 << 40) + 8), 1), (dict(struct_size=10), 1), (dict(k_div=3), 2),
+    (dict(N=40000, k_keep=10, n_seg=1), 2),
+    (dict(kept_feats=(1 << 40) + (1 << 32) + 4096 * 64), 1),  # overlaps vis_feats
+])
+def test_prellm_rejects_before_launch(bad, code):
+    L = trevs.lib()
+    a = _prellm(**bad)
+    assert L.trevs_prellm_workspace_size(ctypes.byref(a)) == 0
+    assert L.trevs_prellm_prune(ctypes.byref(a), None, 0, None) == code
+
+
+def test_prellm_workspace_errors():
+    L = trevs.lib()
+    a = _prellm()
+    need = L.trevs_prellm_workspace_size(ctypes.byref(a))
+    assert L.trevs_prellm_prune(ctypes.byref(a), None, 0, None) == 3
+    assert L.trevs_prellm_prune(ctypes.byref(a), 1 << 44, need - 1, None) == 3
+    assert L.trevs_prellm_prune(ctypes.byref(a), (1 << 44) + 16, need, None) == 3
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(T_max=300), 1), (dict(H_kv=5), 1), (dict(n_keep_heads=0), 1),
+    (dict(n_keep_heads=33), 1), (dict(k_keep=193), 1), (dict(scale=0.0), 1), (dict(P=-1), 1),
+    (dict(hidden_out=None), 1), (dict(d_head=96), 2), (dict(D=4095), 1), (dict(pos=(1 << 40) + 4), 1),
+    (dict(K_in=40000, S=40100, T_max=10), 2),
+    (dict(k_out=(1 << 40) + (1 << 32) + 1024), 1),  # overlaps k
+])
+def test_inllm_rejects_before_launch(bad, code):
+    L = trevs.lib()
+    a = _inllm(**bad)
+    assert L.trevs_inllm_workspace_size(ctypes.byref(a)) == 0
+    assert L.trevs_inllm_prune(ctypes.byref(a), None, 0, None) == code
+
+
+def test_topk_rejects_before_launch():
+    L = trevs.lib()
+    assert L.trevs_topk_select(1 << 40, 1, 10, 11, (1 << 40) + (1 << 32), None, 0, None) == 1
+    assert L.trevs_topk_select(None, 1, 10, 1, (1 << 40) + (1 << 32), None, 0, None) == 1
+    assert L.trevs_topk_select(1 << 40, 1, 40000, 1, (1 << 40) + (1 << 32), None, 0, None) == 2
+    assert L.trevs_topk_select(1 << 40, 1, 10, 5, (1 << 40) + 8, None, 0, None) == 1  # overlap

@@ -1,0 +1,188 @@
+"""Stage 1 (Sec. 4.1, Eq. (2)-(7)) on the GPU through the C ABI, against the
+CPU oracle on the same seeded inputs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_37581_amd import trevs
+from parity import (assert_kept_band, assert_kept_exact_on_own_scores, assert_scores_close,
+                    dev_tensor, host_bits)
+from synthetic import WORKLOADS, stage1_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def run_gpu(inp, w, k_keep=None, **kw):
+    cls = dev_tensor(inp["cls_logits"], w.dtype)
+    Z = dev_tensor(inp["vis_feats"], w.dtype)
+    T = dev_tensor(inp["text_emb"], w.dtype)
+    tl = torch.from_numpy(inp["text_len"]).cuda()
+    call = trevs.Prellm(cls, Z, T, tl, k_keep=k_keep or w.K1, n_seg=w.n_seg,
+                        textual_ratio=w.rho, want_scores=True, **kw)
+    call()
+    torch.cuda.synchronize()
+    return dict(kept_idx=call.kept_idx.cpu().numpy(), kept_feats=host_bits(call.kept_feats),
+                score=call.score.cpu().numpy(), sal=call.sal.cpu().numpy(),
+                rel=call.rel.cpu().numpy(), norm_stats=call.norm_stats.cpu().numpy())
+
+
+def run_oracle(inp, w, k_keep=None, **kw):
+    return oracle.prellm(inp["cls_logits"], inp["vis_feats"], inp["text_emb"], inp["text_len"],
+                         w.dtype, n_seg=w.n_seg, k_keep=k_keep or w.K1, rho=w.rho, **kw)
+
+
+def check(inp, w, g, o, k_keep=None):
+    k = k_keep or w.K1
+    assert_scores_close(g["sal"], o["sal"], "s^v")
+    assert_scores_close(g["rel"], o["rel"], "s^t")
+    ns = np.stack([o["med_v"], o["mad_v"], o["med_t"], o["mad_t"]], axis=1)
+    assert_scores_close(g["norm_stats"], ns, "Med/MAD")
+    assert_scores_close(g["score"], o["score"], "s")
+    assert_kept_band(g["kept_idx"], o["score"], k, "kept")
+    assert_kept_exact_on_own_scores(g["kept_idx"], g["score"], k, "kept")
+    for b in range(w.B):
+        assert np.array_equal(g["kept_feats"][b], inp["vis_feats"][b][g["kept_idx"][b]]), b
+
+
+CASES = {
+    "llava15-b1-f32": WORKLOADS["llava15-b1-f32"],
+    "llava15-b6-bf16-ragged-text": WORKLOADS["llava15-b64-bf16"].with_(B=6),
+    "llavanext-b2-bf16-5tiles": WORKLOADS["llavanext-b16-bf16"].with_(B=2),
+    "qwen25vl-b1-bf16": WORKLOADS["qwen25vl-b4-bf16"].with_(B=1),
+    # ragged everything: N not a multiple of the tile, d with a partial slab,
+    # text rows not a multiple of 32, two [CLS] segments
+    "ragged-bf16": WORKLOADS["llava15-b64-bf16"].with_(
+        B=3, N=200, n_seg=2, d=4104, M_max=40, K1=37, n_sal=3, n_qm=5,
+        text_len=("uniform", 1, 40)),
+    "ragged-f32": WORKLOADS["llava15-b1-f32"].with_(
+        B=2, N=333, n_seg=3, d=1028, M_max=7, K1=111, n_sal=3, n_qm=5),
+    # more text rows than one 128-row chunk
+    "long-text-bf16": WORKLOADS["llava15-b64-bf16"].with_(
+        B=2, N=300, d=512, M_max=150, K1=100, n_sal=4, n_qm=6, text_len=("uniform", 129, 150)),
+    "tie-stress-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=4, tie_stress=True),
+    "rho0-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, rho=0.0),
+    "rho0.25-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, rho=0.25),
+    "rho1-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, rho=1.0),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_stage1_parity(name):
+    w = CASES[name]
+    print(f"[stage1] {name}: B={w.B} N={w.N} d={w.d} M={w.M_max} K1={w.K1} {w.dtype}", flush=True)
+    inp = stage1_inputs(w)
+    g = run_gpu(inp, w)
+    o = run_oracle(inp, w)
+    check(inp, w, g, o)
+
+
+@pytest.mark.parametrize("k", [1, 2, 288, 575, 576])
+def test_stage1_keep_extremes(k):
+    w = WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2)
+    print(f"[stage1] keep {k} of {w.N}", flush=True)
+    inp = stage1_inputs(w)
+    g = run_gpu(inp, w, k_keep=k)
+    o = run_oracle(inp, w, k_keep=k)
+    check(inp, w, g, o, k_keep=k)
+    if k == w.N:
+        assert (g["kept_idx"] == np.arange(w.N)).all()
+
+
+def test_stage1_single_token_and_constant_inputs():
+    w = WORKLOADS["llava15-b1-f32"].with_(B=1, N=1, K1=1, d=64, M_max=3, n_sal=0, n_qm=0)
+    inp = stage1_inputs(w)
+    g = run_gpu(inp, w)
+    assert g["kept_idx"].tolist() == [[0]]
+    # every token identical: all scores tie, the lowest indices win
+    w2 = WORKLOADS["llava15-b1-f32"].with_(B=1, N=64, K1=10, d=64, M_max=3, n_sal=0, n_qm=0)
+    inp2 = stage1_inputs(w2)
+    inp2["cls_logits"][:] = 0.5
+    inp2["vis_feats"][:] = inp2["vis_feats"][:, :1]
+    g2 = run_gpu(inp2, w2)
+    assert g2["kept_idx"].tolist() == [list(range(10))]
+    assert np.all(g2["score"] == 0)
+
+
+def test_stage1_identical_tokens_score_identically():
+    """Position independence: tokens with identical inputs get bit-identical
+    scores wherever they sit in the tiles."""
+    w = WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, tie_stress=True)
+    inp = stage1_inputs(w)
+    g = run_gpu(inp, w)
+    for b in range(w.B):
+        Zb = inp["vis_feats"][b]
+        Lb = inp["cls_logits"][b]
+        keys = {}
+        for i in range(w.N):
+            key = (Zb[i].tobytes(), Lb[:, i].tobytes())
+            keys.setdefault(key, []).append(i)
+        groups = [v for v in keys.values() if len(v) > 1]
+        assert groups
+        for grp in groups:
+            for arr in ("sal", "rel", "score"):
+                vals = g[arr][b, grp]
+                assert np.all(vals == vals[0]), (arr, grp[:4])
+
+
+@pytest.fixture(scope="module")
+def qwen_full():
+    w = WORKLOADS["qwen25vl-b4-bf16"]
+    print(f"[stage1] generating {w.name}", flush=True)
+    return w, stage1_inputs(w)
+
+
+def test_stage1_full_size_qwen_sampled(qwen_full):
+    """The benchmarked launch configuration (B=4, N=16384, d'=3584, M=128):
+    s^v in full, s^t on sampled tokens computed one by one, and every later
+    step re-derived by the oracle from the kernel's own s^v and s^t."""
+    w, inp = qwen_full
+    print("[stage1] full-size qwen", flush=True)
+    g = run_gpu(inp, w)
+    rng = np.random.default_rng(0)
+    for b in range(w.B):
+        sv = oracle.cls_saliency(oracle.to_f64(inp["cls_logits"][b], "bf16"), w.n_seg)
+        assert_scores_close(g["sal"][b], sv, f"s^v[{b}]")
+        idx = np.unique(np.concatenate([rng.choice(w.N, 384, replace=False), inp["matched"][b][:64],
+                                        [0, w.N - 1]]))
+        T = oracle.to_f64(inp["text_emb"][b, :inp["text_len"][b]], "bf16")
+        st = oracle.text_relevance(oracle.to_f64(inp["vis_feats"][b][idx], "bf16"), T)
+        assert_scores_close(g["rel"][b][idx], st, f"s^t[{b}] sampled")
+        gsv = g["sal"][b].astype(np.float64)
+        gst = g["rel"][b].astype(np.float64)
+        hv, med_v, mad_v = oracle.robust_normalise(gsv, 1.4, 1e-8)
+        ht, med_t, mad_t = oracle.robust_normalise(gst, 1.0, 1e-8)
+        assert_scores_close(g["norm_stats"][b], [med_v, mad_v, med_t, mad_t], f"Med/MAD[{b}]")
+        s = oracle.fuse_scores(hv, ht, w.rho, 1.0)
+        assert_scores_close(g["score"][b], s, f"s[{b}]")
+        assert_kept_band(g["kept_idx"][b:b + 1], s[None], w.K1, f"kept[{b}]")
+        assert np.array_equal(g["kept_feats"][b], inp["vis_feats"][b][g["kept_idx"][b]])
+    assert_kept_exact_on_own_scores(g["kept_idx"], g["score"], w.K1, "kept")
+    # planted structure survives: most query-matched tokens are kept
+    for b in range(w.B):
+        assert np.isin(inp["matched"][b], g["kept_idx"][b]).mean() > 0.9
+
+
+def test_stage1_run_to_run_bit_identical(qwen_full):
+    w, inp = qwen_full
+    a = run_gpu(inp, w)
+    b = run_gpu(inp, w)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_stage1_rejects_bad_arguments_without_launching():
+    w = WORKLOADS["llava15-b1-f32"].with_(N=64, K1=8, d=64, M_max=4, n_sal=1, n_qm=1)
+    inp = stage1_inputs(w)
+    cls = dev_tensor(inp["cls_logits"], w.dtype)
+    Z = dev_tensor(inp["vis_feats"], w.dtype)
+    T = dev_tensor(inp["text_emb"], w.dtype)
+    with pytest.raises(trevs.TrevsError) as e:
+        trevs.Prellm(cls, Z, T, k_keep=65)
+    assert e.value.status == 1
+    with pytest.raises(trevs.TrevsError) as e:
+        trevs.Prellm(cls, Z, T, k_keep=8, textual_ratio=1.5)
+    assert e.value.status == 1
+    with pytest.raises(trevs.TrevsError) as e:
+        trevs.Prellm(cls, Z, T, k_keep=8, k_div=2)
+    assert e.value.status == 2

@@ -1,0 +1,153 @@
+"""Stage 2 (Sec. 4.2, Eq. (8)-(9), Top-K_2 and compaction) on the GPU through
+the C ABI, against the CPU oracle on the same seeded inputs."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_37581_amd import trevs
+from parity import (assert_kept_band, assert_kept_exact_on_own_scores, assert_scores_close,
+                    dev_tensor, host_bits)
+from synthetic import WORKLOADS, stage2_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def run_gpu(inp, w, n_keep=None, k_keep=None, use_lse_rest=False):
+    q = dev_tensor(inp["q"], w.dtype)
+    k = dev_tensor(inp["k"], w.dtype)
+    v = dev_tensor(inp["v"], w.dtype)
+    hid = dev_tensor(inp["hidden"], w.dtype)
+    pos = torch.from_numpy(inp["pos"]).cuda()
+    tl = torch.from_numpy(inp["text_len"]).cuda()
+    lr = torch.from_numpy(inp["lse_rest"]).cuda() if use_lse_rest else None
+    call = trevs.Inllm(q, k, v, hid, pos, tl, P=w.P, K_in=w.K1, n_keep_heads=n_keep or w.n_keep,
+                       k_keep=k_keep or w.K2, lse_rest=lr, want_scores=True)
+    call()
+    torch.cuda.synchronize()
+    return dict(kept_idx=call.kept_idx.cpu().numpy(), hidden_out=host_bits(call.hidden_out),
+                k_out=host_bits(call.k_out), v_out=host_bits(call.v_out),
+                pos_out=call.pos_out.cpu().numpy(), head_sel=call.head_sel.cpu().numpy(),
+                head_var=call.head_var.cpu().numpy(), score=call.score.cpu().numpy())
+
+
+def run_oracle(inp, w, n_keep, k_keep, use_lse_rest=False, heads=None):
+    return oracle.inllm(inp["q"], inp["k"], inp["v"], inp["hidden"], inp["pos"], inp["text_len"],
+                        w.dtype, P=w.P, K1=w.K1, n_keep=n_keep, k_keep=k_keep,
+                        scale=1.0 / math.sqrt(w.d_h),
+                        lse_rest=inp["lse_rest"] if use_lse_rest else None, heads=heads)
+
+
+def check(inp, w, g, n_keep=None, k_keep=None, use_lse_rest=False):
+    n_keep = n_keep or w.n_keep
+    k_keep = k_keep or w.K2
+    o = run_oracle(inp, w, n_keep, k_keep, use_lse_rest)
+    assert_scores_close(g["head_var"], o["head_var"], "u_h")
+    assert_kept_band(g["head_sel"], o["head_var"], n_keep, "H*")
+    assert_kept_exact_on_own_scores(g["head_sel"], g["head_var"], n_keep, "H*")
+    if not np.array_equal(g["head_sel"], o["head_sel"]):
+        # heads tied within tolerance: score the oracle with the kernel's head set
+        o = run_oracle(inp, w, n_keep, k_keep, use_lse_rest, heads=g["head_sel"])
+    assert_scores_close(g["score"], o["score"], "p")
+    assert_kept_band(g["kept_idx"], o["score"], k_keep, "kept")
+    assert_kept_exact_on_own_scores(g["kept_idx"], g["score"], k_keep, "kept")
+    S = inp["hidden"].shape[1]
+    for b in range(w.B):
+        rows = oracle.compaction_rows(S, w.P, w.K1, g["kept_idx"][b])
+        assert np.array_equal(g["hidden_out"][b], inp["hidden"][b][rows]), b
+        assert np.array_equal(g["k_out"][b], inp["k"][b][rows]), b
+        assert np.array_equal(g["v_out"][b], inp["v"][b][rows]), b
+        assert np.array_equal(g["pos_out"][:, b], inp["pos"][:, b][:, rows]), b
+    return o
+
+
+CASES = {
+    "llava15-b1-f32": WORKLOADS["llava15-b1-f32"],
+    "llava15-b6-bf16-ragged-text": WORKLOADS["llava15-b64-bf16"].with_(B=6),
+    "llavanext-b2-bf16": WORKLOADS["llavanext-b16-bf16"].with_(B=2),
+    "qwen25vl-b1-bf16-gqa-mrope": WORKLOADS["qwen25vl-b4-bf16"].with_(B=1),
+    # ragged: visual and text rows not multiples of 32, no prefix, GQA 12/3,
+    # d_head 64, odd hidden size
+    "ragged-bf16-dh64": WORKLOADS["llava15-b64-bf16"].with_(
+        B=3, K1=77, K2=20, M_max=45, text_len=("uniform", 1, 45), P=0, H_q=12, H_kv=3,
+        d_h=64, D=200, n_keep=5, n_pos=3, N=400, grid=20),
+    "f32-dh256": WORKLOADS["llava15-b1-f32"].with_(
+        B=2, K1=50, K2=9, M_max=10, H_q=4, H_kv=2, d_h=256, D=48, n_keep=2),
+    "bf16-dh256-mqa": WORKLOADS["llava15-b64-bf16"].with_(
+        B=2, K1=130, K2=30, M_max=33, text_len=("uniform", 20, 33), H_q=8, H_kv=1, d_h=256,
+        D=64, n_keep=3),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_stage2_parity(name):
+    w = CASES[name]
+    print(f"[stage2] {name}: B={w.B} S={w.S} K1={w.K1} T={w.T_max} H={w.H_q}/{w.H_kv} "
+          f"dh={w.d_h} {w.dtype}", flush=True)
+    inp = stage2_inputs(w)
+    g = run_gpu(inp, w)
+    check(inp, w, g)
+
+
+def test_stage2_lse_rest_full_row_softmax():
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=3)
+    print("[stage2] lse_rest", flush=True)
+    inp = stage2_inputs(w, with_lse_rest=True)
+    g = run_gpu(inp, w, use_lse_rest=True)
+    check(inp, w, g, use_lse_rest=True)
+
+
+@pytest.mark.parametrize("n_keep,k_keep", [(32, 64), (1, 64), (16, 192), (16, 1), (4, 11)])
+def test_stage2_keep_extremes(n_keep, k_keep):
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=2)
+    print(f"[stage2] n_keep={n_keep} k_keep={k_keep}", flush=True)
+    inp = stage2_inputs(w)
+    g = run_gpu(inp, w, n_keep=n_keep, k_keep=k_keep)
+    check(inp, w, g, n_keep=n_keep, k_keep=k_keep)
+    if k_keep == w.K1:
+        assert np.array_equal(g["hidden_out"], inp["hidden"])
+    if n_keep == w.H_q:
+        assert (g["head_sel"] == np.arange(w.H_q)).all()
+
+
+@pytest.fixture(scope="module")
+def qwen_full():
+    w = WORKLOADS["qwen25vl-b4-bf16"]
+    print(f"[stage2] generating {w.name}", flush=True)
+    return w, stage2_inputs(w)
+
+
+def test_stage2_full_size_qwen(qwen_full):
+    """The benchmarked launch configuration (B=4, K1=4096, T=128, 28/4 heads)."""
+    w, inp = qwen_full
+    print("[stage2] full-size qwen", flush=True)
+    g = run_gpu(inp, w)
+    check(inp, w, g)
+    # planted structure: the sensitive heads have the highest variance
+    for b in range(w.B):
+        assert np.isin(inp["relevant"][b], g["kept_idx"][b]).mean() > 0.9
+
+
+def test_stage2_run_to_run_bit_identical(qwen_full):
+    w, inp = qwen_full
+    a = run_gpu(inp, w)
+    b = run_gpu(inp, w)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_stage2_rejects_bad_arguments():
+    w = WORKLOADS["llava15-b1-f32"].with_(K1=40, K2=8, M_max=8, H_q=4, H_kv=4, D=32, N=64)
+    inp = stage2_inputs(w)
+    q = dev_tensor(inp["q"], w.dtype)
+    k = dev_tensor(inp["k"], w.dtype)
+    hid = dev_tensor(inp["hidden"], w.dtype)
+    pos = torch.from_numpy(inp["pos"]).cuda()
+    with pytest.raises(trevs.TrevsError) as e:
+        trevs.Inllm(q, k, k.clone(), hid, pos, P=w.P, K_in=w.K1, n_keep_heads=5, k_keep=8)
+    assert e.value.status == 1
+    with pytest.raises(trevs.TrevsError) as e:
+        trevs.Inllm(q, k, k.clone(), hid, pos, P=w.P, K_in=w.K1, n_keep_heads=2, k_keep=41)
+    assert e.value.status == 1
