@@ -57,8 +57,8 @@ typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
 
 /* Implementation limits (TREVS_ERR_UNSUPPORTED beyond them). */
 #define TREVS_MAX_SELECT_N 32768 /* tokens ranked per sample by one top-K */
-#define TREVS_PRELLM_NUM_KERNELS 4 /* prep, relevance, select, gather */
-#define TREVS_INLLM_NUM_KERNELS 5  /* t2v stats, head select, token score, top-K, compaction */
+#define TREVS_PRELLM_NUM_KERNELS 5 /* prep, relevance, robust stats, fuse+top-K, gather */
+#define TREVS_INLLM_NUM_KERNELS 5  /* t2v stats, head variance, head set+token score, top-K, compaction */
 
 /* ------------------------------------------------------------------------
  * Stage 1 (pre-LLM), Sec. 4.1.  Per sample b:

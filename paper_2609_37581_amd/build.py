@@ -30,30 +30,33 @@ def flags():
             "-I", os.path.join(ROOT, "include")]
 
 
-def _compile(src, obj):
-    cmd = [hipcc()] + flags() + ["-c", src, "-o", obj]
+def _compile(src, obj, extra=()):
+    cmd = [hipcc()] + flags() + list(extra) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode:
         raise RuntimeError(f"hipcc failed on {os.path.basename(src)}:\n{r.stderr}")
     return obj
 
 
-def build(verbose=True):
+def build(verbose=True, extra_flags=(), out=LIB):
+    """Compile every HIP source and link `out` (default: the package library).
+    extra_flags are passed to every hipcc compile (e.g. -D tile overrides)."""
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     with tempfile.TemporaryDirectory(prefix="trevs_build_") as tmp:
         objs = [os.path.join(tmp, os.path.basename(s) + ".o") for s in srcs]
         with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-            list(ex.map(_compile, srcs, objs))
-        out = os.path.join(tmp, "libtrevs.so")
-        cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", out] + objs
+            list(ex.map(lambda so: _compile(so[0], so[1], extra_flags), zip(srcs, objs)))
+        dest = out
+        lib_tmp = os.path.join(tmp, "libtrevs.so")
+        cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", lib_tmp] + objs
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode:
             raise RuntimeError("link failed:\n" + r.stderr)
-        shutil.move(out, LIB + ".tmp")
-        os.replace(LIB + ".tmp", LIB)
+        shutil.move(lib_tmp, dest + ".tmp")
+        os.replace(dest + ".tmp", dest)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {dest}")
+    return dest
 
 
 if __name__ == "__main__":

@@ -51,7 +51,7 @@ trevs_status record(void* const* events, int slot, hipStream_t s) {
 
 // ------------------------------------------------------------------ stage 1
 struct PrellmLayout {
-  size_t row_stats, inv_tnorm, sal, rel, total;
+  size_t row_stats, inv_tnorm, sal, rel, stats, total;
 };
 
 trevs_status validate_prellm(const trevs_prellm_args* a) {
@@ -108,6 +108,8 @@ PrellmLayout prellm_layout(const trevs_prellm_args* a) {
   off = align_up(off + (size_t)a->B * a->N * sizeof(float));
   L.rel = off;
   off = align_up(off + (size_t)a->B * a->N * sizeof(float));
+  L.stats = off;
+  off = align_up(off + (size_t)a->B * 4 * sizeof(float));
   L.total = off;
   return L;
 }
@@ -166,25 +168,26 @@ trevs_status validate_inllm(const trevs_inllm_args* a) {
   return TREVS_OK;
 }
 
-// Split of the visual keys for the statistics pass: enough waves to fill the
-// GPU (>= 2048), each split at least 256 keys, split lengths multiples of 32.
+// Split of the visual keys for the statistics pass: enough workgroups to fill
+// the GPU (>= 2 per CU), each split at least 256 keys, lengths multiples of 64
+// (the pass consumes key tiles in pairs of 32).
 InllmPlan inllm_plan(const trevs_inllm_args* a) {
   InllmPlan p;
   const int G = a->H_q / a->H_kv;
   const int nrb = (G * a->T_max + 31) / 32;
-  const int nw = nrb >= 4 ? 4 : (nrb >= 2 ? 2 : 1);
+  const int nw = stats_waves(G, a->T_max);
   p.n_rgroups = (nrb + nw - 1) / nw;
-  const int64_t base_waves = (int64_t)a->B * a->H_kv * nrb;
-  int n_split = (int)std::min<int64_t>((2048 + base_waves - 1) / base_waves, (a->K_in + 255) / 256);
+  const int64_t base_wgs = (int64_t)a->B * a->H_kv * p.n_rgroups;
+  int n_split = (int)std::min<int64_t>((512 + base_wgs - 1) / base_wgs, (a->K_in + 255) / 256);
   n_split = std::max(n_split, 1);
-  p.split_len = ((a->K_in + n_split - 1) / n_split + 31) / 32 * 32;
+  p.split_len = ((a->K_in + n_split - 1) / n_split + 63) / 64 * 64;
   p.n_split = (a->K_in + p.split_len - 1) / p.split_len;
   const size_t rows = (size_t)a->B * a->H_q * a->T_max;
   size_t off = 0;
   p.part = off;
   off = align_up(off + rows * p.n_split * sizeof(float4));
   p.lse2 = off;
-  off = align_up(off + rows * sizeof(float));
+  off = align_up(off + (size_t)a->B * a->H_q * ((a->T_max + 31) / 32 * 32) * sizeof(float));
   p.head_var = off;
   off = align_up(off + (size_t)a->B * a->H_q * sizeof(float));
   p.head_sel = off;
@@ -284,6 +287,8 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   pa.row_bytes = a->d * e;
   pa.inv_tnorm = inv_tnorm;
   pa.n_cls_blocks = a->B * a->H_v * a->n_seg;
+  pa.cls_vec16 = aligned(a->cls_logits, 16) && ((size_t)a->N * e) % 16 == 0 &&
+                 ((size_t)(a->N / a->n_seg) * e) % 16 == 0;
   TREVS_TRY(record(a->events, 0, s));
   TREVS_HIP(launch_prep(pa, a->dtype, s));
   TREVS_TRY(record(a->events, 1, s));
@@ -302,17 +307,29 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   ra.N = a->N;
   ra.M_max = a->M_max;
   ra.row_bytes = a->d * e;
-  ra.tiles_per_sample = (a->N + relevance_tile_tokens() - 1) / relevance_tile_tokens();
+  const int MT = a->M_max <= 32 ? 32 : (a->M_max <= 64 ? 64 : 128);
+  const int tile_tokens = relevance_tile_tokens_for(a->d * e, MT);
+  ra.tiles_per_sample = (a->N + tile_tokens - 1) / tile_tokens;
   ra.sal = sal;
   ra.rel = rel;
-  const int MT = a->M_max <= 32 ? 32 : (a->M_max <= 64 ? 64 : 128);
   TREVS_TRY(record(a->events, 2, s));
   TREVS_HIP(launch_relevance(ra, a->dtype, MT, s));
   TREVS_TRY(record(a->events, 3, s));
 
+  float* stats = reinterpret_cast<float*>(w + L.stats);
+  NormArgs na;
+  na.sal = sal;
+  na.rel = rel;
+  na.N = a->N;
+  na.stats = stats;
+  TREVS_TRY(record(a->events, 4, s));
+  TREVS_HIP(launch_norm_stats(na, a->B, s));
+  TREVS_TRY(record(a->events, 5, s));
+
   SelArgs sa;
   sa.sal = sal;
   sa.rel = rel;
+  sa.stats = stats;
   sa.N = a->N;
   sa.K = a->k_keep;
   sa.wv = (float)(2.0 * (1.0 - (double)a->textual_ratio));
@@ -324,9 +341,9 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   sa.score_out = a->score_out;
   sa.norm_stats = a->norm_stats;
   sa.kept_idx = a->kept_idx;
-  TREVS_TRY(record(a->events, 4, s));
+  TREVS_TRY(record(a->events, 6, s));
   TREVS_HIP(launch_prellm_select(sa, a->B, s));
-  TREVS_TRY(record(a->events, 5, s));
+  TREVS_TRY(record(a->events, 7, s));
 
   GatherArgs ga;
   memset(&ga, 0, sizeof(ga));
@@ -343,9 +360,9 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   ga.P = 0;
   ga.K_in = a->N;
   ga.n_kept = a->k_keep;
-  TREVS_TRY(record(a->events, 6, s));
+  TREVS_TRY(record(a->events, 8, s));
   TREVS_HIP(launch_gather(ga, s));
-  TREVS_TRY(record(a->events, 7, s));
+  TREVS_TRY(record(a->events, 9, s));
   return TREVS_OK;
 }
 
@@ -361,7 +378,6 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   float4* part = reinterpret_cast<float4*>(w + p.part);
   float* lse2 = reinterpret_cast<float*>(w + p.lse2);
   float* head_var = a->head_var ? a->head_var : reinterpret_cast<float*>(w + p.head_var);
-  int32_t* head_sel = a->head_sel ? a->head_sel : reinterpret_cast<int32_t*>(w + p.head_sel);
   float* score = a->score_out ? a->score_out : reinterpret_cast<float*>(w + p.score);
 
   StatsArgs ta;
@@ -389,14 +405,13 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   ha.B = a->B;
   ha.H_q = a->H_q;
   ha.T_max = a->T_max;
+  ha.T_pad = (a->T_max + 31) / 32 * 32;
   ha.K_in = a->K_in;
   ha.n_split = p.n_split;
-  ha.n_keep = a->n_keep_heads;
   ha.text_len = a->text_len;
   ha.lse_rest = a->lse_rest;
   ha.lse2 = lse2;
   ha.head_var = head_var;
-  ha.head_sel = head_sel;
   TREVS_TRY(record(a->events, 2, s));
   TREVS_HIP(launch_heads(ha, s));
   TREVS_TRY(record(a->events, 3, s));
@@ -409,13 +424,16 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   sa.P = a->P;
   sa.K_in = a->K_in;
   sa.T_max = a->T_max;
+  sa.T_pad = (a->T_max + 31) / 32 * 32;
   sa.H_q = a->H_q;
   sa.H_kv = a->H_kv;
   sa.G = G;
   sa.n_keep = a->n_keep_heads;
+  sa.n_vtiles = (a->K_in + score_tile_tokens(a->dtype, a->d_head) - 1) / score_tile_tokens(a->dtype, a->d_head);
   sa.scale_log2e = scale_log2e;
   sa.lse2 = lse2;
-  sa.head_sel = head_sel;
+  sa.head_var = head_var;
+  sa.head_sel = a->head_sel;
   sa.text_len = a->text_len;
   sa.p = score;
   TREVS_TRY(record(a->events, 4, s));

@@ -16,6 +16,7 @@ struct PrepArgs {
   int M_max, row_bytes;      // row_bytes = d * elem
   float* inv_tnorm;          // [B*M_max]: 1/max(||t_j||, 1e-12), 0 for j >= M_b
   int n_cls_blocks;          // blocks [0, n_cls_blocks) do [CLS] rows, the rest text rows
+  int cls_vec16;             // every [CLS] segment row starts 16-byte aligned
 };
 
 struct RelArgs {
@@ -31,9 +32,17 @@ struct RelArgs {
   float* rel;                // [B,N]
 };
 
+struct NormArgs {
+  const float* sal;
+  const float* rel;
+  int N;
+  float* stats;              // [B,4]: Med(s^v), MAD(s^v), Med(s^t), MAD(s^t)
+};
+
 struct SelArgs {
   const float* sal;
   const float* rel;
+  const float* stats;        // [B,4] from the robust-statistics kernel
   int N, K;
   float wv, wt, tau_v, tau_t, lam, eps;
   float* score_out;          // [B,N] or null
@@ -54,21 +63,22 @@ struct StatsArgs {
 
 struct HeadArgs {
   const float4* part;
-  int B, H_q, T_max, K_in, n_split, n_keep;
+  int B, H_q, T_max, T_pad, K_in, n_split;
   const int32_t* text_len;
   const float* lse_rest;     // [B,H_q,T_max] natural log, or null
-  float* lse2;               // [B,H_q,T_max] row log-sum-exp in log2 units
-  float* head_var;           // [B,H_q]
-  int32_t* head_sel;         // [B,n_keep]
+  float* lse2;               // [B,H_q,T_pad] row log-sum-exp in log2 units (T_pad = T_max rounded up to 32)
+  float* head_var;           // [B,H_q] u_h
 };
 
 struct ScoreArgs {
   const void* q;
   const void* k;
-  int B, S, P, K_in, T_max, H_q, H_kv, G, n_keep;
+  int B, S, P, K_in, T_max, T_pad, H_q, H_kv, G, n_keep;
+  int n_vtiles;              // workgroups per sample (score_tile_tokens visual tokens each)
   float scale_log2e;
   const float* lse2;
-  const int32_t* head_sel;
+  const float* head_var;     // [B,H_q] u_h
+  int32_t* head_sel;         // [B,n_keep] H* ascending, or null
   const int32_t* text_len;
   float* p;                  // [B,K_in]
 };
@@ -97,6 +107,9 @@ constexpr int kGatherThreads = 256;
 hipError_t launch_prep(const PrepArgs& a, int dtype, hipStream_t s);
 hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s);
 int relevance_tile_tokens();
+// Tokens per workgroup of the relevance launch for this row size / text tile.
+int relevance_tile_tokens_for(int row_bytes, int MT);
+hipError_t launch_norm_stats(const NormArgs& a, int B, hipStream_t s);
 hipError_t launch_prellm_select(const SelArgs& a, int B, hipStream_t s);
 hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, hipStream_t s);
 hipError_t launch_stats(const StatsArgs& a, int dtype, int dh, hipStream_t s);
@@ -104,7 +117,9 @@ hipError_t launch_heads(const HeadArgs& a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs& a, int dtype, int dh, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 
-// Number of 32-row text blocks the token-score kernel handles per workgroup.
-int score_qblocks(int T_max);
+// Waves per workgroup of the statistics pass (column blocks of 32 rows).
+int stats_waves(int G, int T_max);
+// Visual tokens per workgroup of the token-score pass.
+int score_tile_tokens(int dtype, int dh);
 
 }  // namespace trevs

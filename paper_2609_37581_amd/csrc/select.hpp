@@ -1,27 +1,28 @@
-// Workgroup-wide exact order statistics and stable top-K (one workgroup of
-// 512 threads per sample; thread t owns the E consecutive elements
-// [t*E, t*E + E), so a workgroup prefix sum walks the elements in index order).
+// Workgroup-wide exact order statistics and stable top-K.  One workgroup of
+// 1024 threads ranks one vector; thread t owns the E consecutive elements
+// [t*E, t*E + E), so a workgroup prefix sum walks the elements in index order.
 #pragma once
 
 #include "common.hpp"
 
 namespace trevs {
 
-constexpr int kSelThreads = 512;
+constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
-constexpr int kRadixBits = 8;
-constexpr int kRadixBins = 1 << kRadixBits;
+constexpr int kFirstBits = 11;                // digit width of the first radix pass
+constexpr int kFirstBins = 1 << kFirstBits;
+constexpr int kLaterBits = 8;                 // digit width of the candidate passes
+constexpr int kCandCap = 4096;                // candidates kept in LDS after the first pass
 
 struct SelectShared {
-  uint32_t hist[2][kRadixBins];
-  uint32_t mn[2][kSelWaves];
-  uint32_t mx[2][kSelWaves];
+  uint32_t hist[kFirstBins];
+  uint32_t cand[kCandCap];
+  uint32_t mn[kSelWaves];
+  uint32_t mx[kSelWaves];
   int wave_tot[kSelWaves];
   int wave_excl[kSelWaves];
   int total;
-  uint32_t res_digit[2];
-  uint32_t res_before[2];
-  uint32_t res_count[2];
+  uint32_t res_digit, res_before, res_count;
 };
 
 // Exclusive prefix sum of one int per thread over the workgroup.
@@ -43,125 +44,193 @@ __device__ __forceinline__ int block_excl_scan(int v, SelectShared& sh, int& tot
   return r;
 }
 
-// Histogram increment with wave aggregation of the first active lane's
-// digit (many lanes share one digit when values cluster, e.g. exact zeros).
-__device__ __forceinline__ void hist_add(uint32_t* hist, bool act, uint32_t digit, int lane) {
+// Histogram increment.  The lanes that share the first active lane's digit
+// are counted with one atomic (values cluster, e.g. exact zeros, which would
+// otherwise serialise on one LDS address); the others add one each.  Must be
+// called by every lane of the wave.
+__device__ __forceinline__ void hist_add(uint32_t* hist, bool act, uint32_t digit) {
   const unsigned long long am = __ballot(act);
   if (am == 0ull) return;
   const int leader = __ffsll((long long)am) - 1;
-  const uint32_t d0 = (uint32_t)__shfl((int)digit, leader, kWave);
+  const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)digit, leader);
   const unsigned long long same = __ballot(act && digit == d0);
-  if (lane == leader) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
+  if ((int)(threadIdx.x & (kWave - 1)) == leader) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
   if (act && digit != d0) atomicAdd(&hist[digit], 1u);
 }
 
-// Exact rank selection on uint32 keys for NSET independent key sets at once.
-// keyf(s, e) yields the key of this thread's element e in set s (recomputed
-// on every pass rather than held in registers).  For set s returns the key of
-// ascending 0-based rank rank[s] among the N valid keys, the number of keys
-// strictly below it, and the number equal to it.  Radix passes of 8 bits
-// start below the common prefix of the set's minimum and maximum key.
-template <int NSET, int E, class KeyF>
-__device__ void block_select(KeyF keyf, int base, int N, const int (&rank)[NSET],
-                             uint32_t (&res)[NSET], int (&less)[NSET], int (&eq)[NSET],
-                             SelectShared& sh) {
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  uint32_t mn[NSET], mx[NSET];
+// Finds the bin holding rank krem in hist[0, nbins): every thread owns two
+// bins, a workgroup scan orders them.  Result in sh.res_*.
+__device__ __forceinline__ void block_find_bin(int nbins, int krem, SelectShared& sh) {
+  const int t = threadIdx.x;
+  const int c0 = 2 * t < nbins ? (int)sh.hist[2 * t] : 0;
+  const int c1 = 2 * t + 1 < nbins ? (int)sh.hist[2 * t + 1] : 0;
+  int tot;
+  const int excl = block_excl_scan(c0 + c1, sh, tot);
+  if (excl <= krem && krem < excl + c0 + c1) {
+    const bool first = krem < excl + c0;
+    sh.res_digit = 2 * t + (first ? 0 : 1);
+    sh.res_before = first ? excl : excl + c0;
+    sh.res_count = first ? c0 : c1;
+  }
+  __syncthreads();
+}
+
+// Finds the bin holding rank krem in hist[0, 256) with wave 0 alone.
+__device__ __forceinline__ void wave0_find_bin(int krem, SelectShared& sh) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (threadIdx.x < kWave) {
+    uint32_t c[4];
+    int lsum = 0;
 #pragma unroll
-  for (int s = 0; s < NSET; ++s) {
-    mn[s] = 0xffffffffu;
-    mx[s] = 0u;
+    for (int j = 0; j < 4; ++j) {
+      c[j] = sh.hist[4 * lane + j];
+      lsum += (int)c[j];
+    }
+    const int excl = wave_incl_scan(lsum, lane) - lsum;
+    if (excl <= krem && krem < excl + lsum) {
+      int run = excl;
 #pragma unroll
-    for (int e = 0; e < E; ++e)
-      if (base + e < N) {
-        const uint32_t k = keyf(s, e);
-        mn[s] = min(mn[s], k);
-        mx[s] = max(mx[s], k);
+      for (int j = 0; j < 4; ++j) {
+        if (krem < run + (int)c[j]) {
+          sh.res_digit = 4 * lane + j;
+          sh.res_before = run;
+          sh.res_count = c[j];
+          break;
+        }
+        run += (int)c[j];
       }
-    mn[s] = wave_min_u32(mn[s]);
-    mx[s] = wave_max_u32(mx[s]);
-    if (lane == 0) {
-      sh.mn[s][wave] = mn[s];
-      sh.mx[s][wave] = mx[s];
     }
   }
   __syncthreads();
-  int nb[NSET], krem[NSET];
-  uint32_t prefix[NSET];
+}
+
+// Exact rank selection on uint32 keys.  keyf(e) yields the key of this
+// thread's element e (recomputed on demand, not held).  Returns the key of
+// ascending 0-based rank `rank` among the N valid keys, with the number of
+// keys strictly below it (less) and equal to it (eq).
+//   1. min and max; the bits above their highest differing bit are common.
+//   2. one pass over all elements on the next (up to) 11 bits;
+//   3. the elements in the chosen bin are compacted into LDS (if they fit)
+//      and the remaining bits are resolved 8 at a time over them alone;
+//      otherwise the remaining passes scan all elements.
+template <int E, class KeyF>
+__device__ void block_select(KeyF keyf, int base, int N, int rank, uint32_t& res, int& less,
+                             int& eq, SelectShared& sh) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  uint32_t mn = 0xffffffffu, mx = 0u;
 #pragma unroll
-  for (int s = 0; s < NSET; ++s) {
-    uint32_t a = 0xffffffffu, z = 0u;
-    for (int w = 0; w < kSelWaves; ++w) {
-      a = min(a, sh.mn[s][w]);
-      z = max(z, sh.mx[s][w]);
+  for (int e = 0; e < E; ++e)
+    if (base + e < N) {
+      const uint32_t k = keyf(e);
+      mn = min(mn, k);
+      mx = max(mx, k);
     }
-    const uint32_t diff = a ^ z;
-    nb[s] = diff ? 32 - __clz(diff) : 0;
-    prefix[s] = (uint32_t)(((uint64_t)a >> nb[s]) << nb[s]);
-    krem[s] = rank[s];
-    less[s] = 0;
-    eq[s] = diff ? 0 : N;
+  mn = wave_min_u32(mn);
+  mx = wave_max_u32(mx);
+  if (lane == 0) {
+    sh.mn[wave] = mn;
+    sh.mx[wave] = mx;
+  }
+  __syncthreads();
+  uint32_t a = 0xffffffffu, z = 0u;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    a = min(a, sh.mn[w]);
+    z = max(z, sh.mx[w]);
   }
   __syncthreads();  // sh.mn / sh.mx are rewritten by the next call
-  for (;;) {
-    bool any = false;
-#pragma unroll
-    for (int s = 0; s < NSET; ++s) any |= nb[s] > 0;
-    if (!any) break;
-    for (int i = tid; i < NSET * kRadixBins; i += kSelThreads) sh.hist[i / kRadixBins][i % kRadixBins] = 0u;
+  const uint32_t diff = a ^ z;
+  less = 0;
+  if (diff == 0u) {
+    res = a;
+    eq = N;
+    return;
+  }
+  int nb = 32 - __clz(diff);
+  uint32_t prefix = (uint32_t)(((uint64_t)a >> nb) << nb);
+  int krem = rank;
+
+  // ---- first pass: every element shares the prefix above bit nb
+  {
+    const int db = min(kFirstBits, nb), shift = nb - db;
+    const uint32_t dmask = (1u << db) - 1u;
+    for (int i = tid; i < (1 << db); i += kSelThreads) sh.hist[i] = 0u;
     __syncthreads();
 #pragma unroll
-    for (int s = 0; s < NSET; ++s) {
-      if (nb[s] == 0) continue;
-      const int db = min(kRadixBits, nb[s]), shift = nb[s] - db;
+    for (int e = 0; e < E; ++e) hist_add(sh.hist, base + e < N, (keyf(e) >> shift) & dmask);
+    __syncthreads();
+    block_find_bin(1 << db, krem, sh);
+    prefix |= sh.res_digit << shift;
+    krem -= (int)sh.res_before;
+    less += (int)sh.res_before;
+    nb = shift;
+    eq = (int)sh.res_count;
+  }
+  if (nb == 0) {
+    res = prefix;
+    return;
+  }
+  const int ncand = eq;
+  if (ncand <= kCandCap) {
+    // ---- compact the candidates (keys sharing the prefix above bit nb)
+    int mine = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      mine += (base + e < N && ((uint64_t)keyf(e) >> nb) == ((uint64_t)prefix >> nb)) ? 1 : 0;
+    int tot;
+    int off = block_excl_scan(mine, sh, tot);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const uint32_t k = keyf(e);
+      if (base + e < N && ((uint64_t)k >> nb) == ((uint64_t)prefix >> nb) && off < kCandCap)
+        sh.cand[off++] = k;
+    }
+    __syncthreads();
+    const int rounds = (ncand + kSelThreads - 1) / kSelThreads;
+    while (nb > 0) {
+      const int db = min(kLaterBits, nb), shift = nb - db;
       const uint32_t dmask = (1u << db) - 1u;
+      if (tid < (1 << kLaterBits)) sh.hist[tid] = 0u;
+      __syncthreads();
+      for (int r = 0; r < rounds; ++r) {
+        const int c = r * kSelThreads + tid;
+        const uint32_t k = c < ncand ? sh.cand[c] : 0u;
+        const bool act = c < ncand && ((uint64_t)k >> nb) == ((uint64_t)prefix >> nb);
+        hist_add(sh.hist, act, (k >> shift) & dmask);
+      }
+      __syncthreads();
+      wave0_find_bin(krem, sh);
+      prefix |= sh.res_digit << shift;
+      krem -= (int)sh.res_before;
+      less += (int)sh.res_before;
+      eq = (int)sh.res_count;
+      nb = shift;
+      __syncthreads();  // sh.res_* and sh.hist are rewritten next round
+    }
+  } else {
+    // ---- many keys share the first digit: resolve the rest over all elements
+    while (nb > 0) {
+      const int db = min(kLaterBits, nb), shift = nb - db;
+      const uint32_t dmask = (1u << db) - 1u;
+      if (tid < (1 << kLaterBits)) sh.hist[tid] = 0u;
+      __syncthreads();
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        const uint32_t k = keyf(s, e);
-        const bool match = ((uint64_t)k >> nb[s]) == ((uint64_t)prefix[s] >> nb[s]);
-        hist_add(sh.hist[s], base + e < N && match, (k >> shift) & dmask, lane);
+        const uint32_t k = keyf(e);
+        const bool act = base + e < N && ((uint64_t)k >> nb) == ((uint64_t)prefix >> nb);
+        hist_add(sh.hist, act, (k >> shift) & dmask);
       }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int s = 0; s < NSET; ++s) {
-      if (wave != s || nb[s] == 0) continue;
-      uint32_t c[4];
-      int lsum = 0;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        c[j] = sh.hist[s][4 * lane + j];
-        lsum += (int)c[j];
-      }
-      const int excl = wave_incl_scan(lsum, lane) - lsum;
-      if (excl <= krem[s] && krem[s] < excl + lsum) {
-        int run = excl;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (krem[s] < run + (int)c[j]) {
-            sh.res_digit[s] = 4 * lane + j;
-            sh.res_before[s] = run;
-            sh.res_count[s] = c[j];
-            break;
-          }
-          run += (int)c[j];
-        }
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int s = 0; s < NSET; ++s) {
-      if (nb[s] == 0) continue;
-      const int db = min(kRadixBits, nb[s]), shift = nb[s] - db;
-      prefix[s] |= sh.res_digit[s] << shift;
-      krem[s] -= (int)sh.res_before[s];
-      less[s] += (int)sh.res_before[s];
-      nb[s] = shift;
-      if (shift == 0) eq[s] = (int)sh.res_count[s];
+      __syncthreads();
+      wave0_find_bin(krem, sh);
+      prefix |= sh.res_digit << shift;
+      krem -= (int)sh.res_before;
+      less += (int)sh.res_before;
+      eq = (int)sh.res_count;
+      nb = shift;
+      __syncthreads();
     }
   }
-#pragma unroll
-  for (int s = 0; s < NSET; ++s) res[s] = prefix[s];
+  res = prefix;
 }
 
 // Stable top-K: keep every element whose score is above the K-th largest and
@@ -170,32 +239,32 @@ __device__ void block_select(KeyF keyf, int base, int N, const int (&rank)[NSET]
 template <int E>
 __device__ void block_topk_write(const float (&sc)[E], int base, int N, int K, int32_t* out,
                                  SelectShared& sh) {
-  auto keyf = [&](int, int e) { return f2key(sc[e]); };
-  const int rank[1] = {N - K};
-  uint32_t res[1];
-  int less[1], eq[1];
-  block_select<1, E>(keyf, base, N, rank, res, less, eq, sh);
-  const uint32_t thr = res[0];
-  const int need_eq = K - (N - less[0] - eq[0]);
+  auto keyf = [&](int e) { return f2key(sc[e]); };
+  uint32_t thr;
+  int less, eq;
+  block_select<E>(keyf, base, N, N - K, thr, less, eq, sh);
+  const int need_eq = K - (N - less - eq);
   int my_eq = 0;
 #pragma unroll
-  for (int e = 0; e < E; ++e) my_eq += (base + e < N && f2key(sc[e]) == thr) ? 1 : 0;
+  for (int e = 0; e < E; ++e) my_eq += (base + e < N && keyf(e) == thr) ? 1 : 0;
   int tot;
   int run = block_excl_scan(my_eq, sh, tot);
-  bool keep[E];
+  uint32_t keep_mask = 0u;
   int my_keep = 0;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const bool valid = base + e < N;
-    const bool is_eq = valid && f2key(sc[e]) == thr;
-    keep[e] = valid && (f2key(sc[e]) > thr || (is_eq && run < need_eq));
+    const uint32_t k = keyf(e);
+    const bool is_eq = valid && k == thr;
+    const bool keep = valid && (k > thr || (is_eq && run < need_eq));
     run += is_eq ? 1 : 0;
-    my_keep += keep[e] ? 1 : 0;
+    keep_mask |= keep ? (1u << e) : 0u;
+    my_keep += keep ? 1 : 0;
   }
   int pos = block_excl_scan(my_keep, sh, tot);
 #pragma unroll
   for (int e = 0; e < E; ++e)
-    if (keep[e] && pos < K) out[pos++] = base + e;  // exactly K are kept; the bound only guards memory
+    if (((keep_mask >> e) & 1u) && pos < K) out[pos++] = base + e;  // exactly K kept; bound guards memory
 }
 
 }  // namespace trevs

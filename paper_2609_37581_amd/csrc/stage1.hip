@@ -7,35 +7,96 @@
 namespace trevs {
 
 // ---------------------------------------------------------------------------
-// Prep: per ([CLS] head, segment) softmax statistics, and per text row the
-// inverse L2 norm.  Blocks [0, n_cls_blocks) take one [CLS] row each; every
-// later block takes 4 text rows, one per wave.
+// Prep.  Blocks [0, n_cls_blocks) take one ([CLS] head, segment) row each and
+// reduce it in one pass to its softmax statistics (max and sum of exp, log2
+// units, Eq. (2)); every later block takes 8 text rows, one per wave, and
+// stores the inverse L2 norm of each (Sec. 4.1, before Eq. (4)).
 // ---------------------------------------------------------------------------
+constexpr int kPrepThreads = 512;
+
+__device__ __forceinline__ void online_merge(float& m, float& s, float mo, float so) {
+  const float mn = fmaxf(m, mo);
+  if (mn == -INFINITY) return;
+  s = s * __builtin_amdgcn_exp2f(m - mn) + so * __builtin_amdgcn_exp2f(mo - mn);
+  m = mn;
+}
+
 template <class In>
-__global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
-  __shared__ float red[4];
+__device__ __forceinline__ void online_vec(float& m, float& s, u32x4 w);
+template <>
+__device__ __forceinline__ void online_vec<BF16>(float& m, float& s, u32x4 w) {
+  float x[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    x[2 * j] = bf16_lo(w[j]) * kLog2e;
+    x[2 * j + 1] = bf16_hi(w[j]) * kLog2e;
+  }
+  float vm = x[0];
+#pragma unroll
+  for (int j = 1; j < 8; ++j) vm = fmaxf(vm, x[j]);
+  const float mn = fmaxf(m, vm);
+  float acc = s * __builtin_amdgcn_exp2f(m - mn);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc += __builtin_amdgcn_exp2f(x[j] - mn);
+  s = acc;
+  m = mn;
+}
+template <>
+__device__ __forceinline__ void online_vec<F32>(float& m, float& s, u32x4 w) {
+  float x[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = __uint_as_float(w[j]) * kLog2e;
+  const float vm = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+  const float mn = fmaxf(m, vm);
+  float acc = s * __builtin_amdgcn_exp2f(m - mn);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc += __builtin_amdgcn_exp2f(x[j] - mn);
+  s = acc;
+  m = mn;
+}
+
+template <class In>
+__global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
+  constexpr int NWV = kPrepThreads / 64;
+  __shared__ float red_m[NWV], red_s[NWV];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if ((int)blockIdx.x < a.n_cls_blocks) {
     const int row = blockIdx.x;  // = (b*H + h)*n_seg + seg
     const int seg = row % a.n_seg, bh = row / a.n_seg;
     const size_t base = (size_t)bh * a.N + (size_t)seg * a.seg_len;
-    float m = -INFINITY;
-    for (int i = tid; i < a.seg_len; i += 256) m = fmaxf(m, load_scalar(a.cls, base + i, In{}));
-    m = wave_max(m);
-    if (lane == 0) red[wave] = m;
+    float m = -INFINITY, s = 0.f;
+    if (a.cls_vec16) {
+      const uint8_t* p = reinterpret_cast<const uint8_t*>(a.cls) + base * In::kBytes;
+      const int nvec = a.seg_len * In::kBytes / 16;
+      for (int v = tid; v < nvec; v += 4 * kPrepThreads) {
+        u32x4 w[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          w[u] = v + u * kPrepThreads < nvec ? ldg16(p + (size_t)(v + u * kPrepThreads) * 16) : zero4();
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (v + u * kPrepThreads < nvec) online_vec<In>(m, s, w[u]);
+      }
+    } else {
+      for (int i = tid; i < a.seg_len; i += kPrepThreads) {
+        const float x = load_scalar(a.cls, base + i, In{}) * kLog2e;
+        online_merge(m, s, x, 1.f);
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) online_merge(m, s, __shfl_xor(m, o, 64), __shfl_xor(s, o, 64));
+    if (lane == 0) {
+      red_m[wave] = m;
+      red_s[wave] = s;
+    }
     __syncthreads();
-    m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])) * kLog2e;
-    __syncthreads();
-    float s = 0.f;
-    for (int i = tid; i < a.seg_len; i += 256)
-      s += exp2f(fmaf(load_scalar(a.cls, base + i, In{}), kLog2e, -m));
-    s = wave_sum(s);
-    if (lane == 0) red[wave] = s;
-    __syncthreads();
-    if (tid == 0) a.row_stats[row] = make_float2(m, 1.f / ((red[0] + red[1]) + (red[2] + red[3])));
+    if (tid == 0) {
+      for (int w = 1; w < NWV; ++w) online_merge(m, s, red_m[w], red_s[w]);
+      a.row_stats[row] = make_float2(m, 1.f / s);
+    }
     return;
   }
-  const int r = ((int)blockIdx.x - a.n_cls_blocks) * 4 + wave;  // = b*M_max + j
+  const int r = ((int)blockIdx.x - a.n_cls_blocks) * NWV + wave;  // = b*M_max + j
   if (r >= a.B * a.M_max) return;
   const int b = r / a.M_max, j = r - b * a.M_max;
   const int Mb = a.text_len ? a.text_len[b] : a.M_max;
@@ -43,7 +104,13 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   if (j < Mb) {
     const uint8_t* row = reinterpret_cast<const uint8_t*>(a.text) + (size_t)r * a.row_bytes;
     float s = 0.f;
-    for (int off = lane * 16; off < a.row_bytes; off += 64 * 16) s += sumsq(ldg16(row + off), In{});
+    for (int off = lane * 16; off < a.row_bytes; off += 4 * 64 * 16) {
+      u32x4 w[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) w[u] = off + u * 1024 < a.row_bytes ? ldg16(row + off + u * 1024) : zero4();
+#pragma unroll
+      for (int u = 0; u < 4; ++u) s += sumsq(w[u], In{});
+    }
     s = wave_sum(s);
     inv = 1.f / fmaxf(sqrtf(s), 1e-12f);
   }
@@ -51,27 +118,40 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Relevance: one pass over the visual features Z.  A workgroup owns VT
-// consecutive visual tokens of one sample; each wave owns NB blocks of 32
-// tokens and computes C[text j][token i] = t_j . z_i on the matrix cores
-// (text tile from LDS, Z straight from HBM into registers, 128-byte row
-// slabs double buffered).  The same Z registers give ||z_i||^2; the epilogue
-// applies the norms, rectifies, squares and averages over the valid text
-// rows (Eq. (4)-(5)).  The workgroup also finishes the head-mean saliency of
-// its tokens from the prep statistics (Eq. (2)-(3)).
+// Relevance: one pass over the visual features Z.  A workgroup owns 32*NW
+// consecutive visual tokens of one sample; each wave owns 32 of them and
+// computes C[text j][token i] = t_j . z_i on the matrix cores, streaming the
+// feature dimension in slabs of SB bytes per row: the text slab goes through
+// LDS (shared by the waves), each wave's Z rows go straight from HBM into
+// registers.  Two register/LDS buffers alternate (A computes while B loads);
+// every load is issued unconditionally (out-of-range lanes read an
+// L2-resident dummy row and are masked where the data is used) so that the
+// compiler can wait for exactly the older buffer.  The same Z registers give
+// ||z_i||^2; the epilogue applies the norms, rectifies, squares and averages
+// over the valid text rows (Eq. (4)-(5)).  The workgroup also finishes the
+// head-mean saliency of its tokens from the prep statistics (Eq. (2)-(3)).
 // ---------------------------------------------------------------------------
-constexpr int kRelNB = 1;
-constexpr int kRelNW = 4;
-constexpr int kLdsRow = 128 + 16;  // padded LDS row stride (bytes) of a 128-byte text slab row
+#ifndef TREVS_REL_NW
+#define TREVS_REL_NW 4
+#endif
+#ifndef TREVS_REL_SB
+#define TREVS_REL_SB 256
+#endif
+constexpr int kRelNW = TREVS_REL_NW;
+constexpr int kRelSB = TREVS_REL_SB;
 
-template <class In, int MT, int NB, int NW>
+template <class In, int MT, int NW, int SB>
 __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
   constexpr int MB = MT / 32;
   constexpr int NT = 64 * NW;
-  constexpr int VT = 32 * NB * NW;
-  constexpr int TV = MT * 8;  // 16-byte vectors in one text slab
+  constexpr int VT = 32 * NW;
+  constexpr int NF = SB / 128;       // 64-byte fragments per lane per slab
+  constexpr int HS = SB / 2;         // bytes of a slab row carried by one lane half
+  constexpr int LROW = SB + 16;      // padded LDS row stride
+  constexpr int CPR = SB / 16;       // 16-byte vectors per slab row
+  constexpr int TV = MT * CPR;       // 16-byte vectors per text slab
   constexpr int TVT = (TV + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) uint8_t tlds[2][MT * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint8_t tlds[2][MT * LROW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
@@ -80,7 +160,8 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
   const int tok0 = (tile - b * a.tiles_per_sample) * VT;
   const int N = a.N, rb = a.row_bytes;
   const int Mb = a.text_len ? a.text_len[b] : a.M_max;
-  const int n_slabs = (rb + 127) >> 7;
+  const int n_slabs = (rb + SB - 1) / SB;
+  const int n_pairs = (n_slabs + 1) / 2;
 
   // ---- saliency of this tile's tokens
   for (int t = tid; t < VT; t += NT) {
@@ -91,97 +172,95 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
       for (int h = 0; h < a.H; ++h) {
         const float2 st = a.row_stats[((size_t)b * a.H + h) * a.n_seg + seg];
         const float x = load_scalar(a.cls, ((size_t)b * a.H + h) * N + i, In{});
-        acc = fmaf(exp2f(fmaf(x, kLog2e, -st.x)), st.y, acc);
+        acc = fmaf(__builtin_amdgcn_exp2f(fmaf(x, kLog2e, -st.x)), st.y, acc);
       }
       a.sal[(size_t)b * N + i] = acc / (float)a.H;
     }
   }
 
-  // ---- visual rows carried by this lane
-  const uint8_t* zrow[NB];
-  bool zvalid[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int i = tok0 + (wave * NB + nb) * 32 + col;
-    zvalid[nb] = i < N;
-    zrow[nb] = reinterpret_cast<const uint8_t*>(a.Z) + ((size_t)b * N + (zvalid[nb] ? i : N - 1)) * rb +
-               half * 64;
-  }
+  const int tok = tok0 + wave * 32 + col;
+  const bool tok_ok = tok < N;
   const uint8_t* tbase = reinterpret_cast<const uint8_t*>(a.T) + (size_t)b * a.M_max * rb;
+  const uint8_t* dummy = tbase;  // always valid and hot in L2
+  const uint8_t* zrow = reinterpret_cast<const uint8_t*>(a.Z) +
+                        ((size_t)b * N + (tok_ok ? tok : N - 1)) * rb + half * HS;
 
-  auto load_z = [&](int s, u32x4 (&dst)[NB][4]) {
+  auto load_z = [&](int s, u32x4 (&dst)[NF][4]) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int f = 0; f < NF; ++f)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int off = s * 128 + q * 16;
-        dst[nb][q] = (off + half * 64 < rb) ? ldg16_stream(zrow[nb] + off) : zero4();
+        const int off = s * SB + f * 64 + q * 16;
+        dst[f][q] = ldg16_stream(off + half * HS < rb ? zrow + off : dummy);
       }
   };
   auto load_t = [&](int s, int j0, u32x4 (&dst)[TVT]) {
 #pragma unroll
     for (int k = 0; k < TVT; ++k) {
-      const int v = tid + k * NT, row = v >> 3, c = v & 7;
-      const int off = s * 128 + c * 16;
-      dst[k] = (v < TV && j0 + row < Mb && off < rb) ? ldg16(tbase + (size_t)(j0 + row) * rb + off)
-                                                     : zero4();
+      const int v = min(tid + k * NT, TV - 1), row = v / CPR, c = v - row * CPR;
+      const int off = s * SB + c * 16;
+      const bool ok = j0 + row < Mb && off < rb;
+      dst[k] = ldg16(ok ? tbase + (size_t)(j0 + row) * rb + off : dummy);
     }
   };
-  auto store_t = [&](int buf, const u32x4 (&src)[TVT]) {
+  auto store_t = [&](int buf, int s, int j0, const u32x4 (&src)[TVT]) {
 #pragma unroll
     for (int k = 0; k < TVT; ++k) {
-      const int v = tid + k * NT, row = v >> 3, c = v & 7;
-      if (v < TV) *reinterpret_cast<u32x4*>(&tlds[buf][row * kLdsRow + c * 16]) = src[k];
+      const int v = tid + k * NT;
+      if (v < TV) {
+        const int row = v / CPR, c = v - row * CPR;
+        const bool ok = j0 + row < Mb && s * SB + c * 16 < rb;
+        *reinterpret_cast<u32x4*>(&tlds[buf][row * LROW + c * 16]) = ok ? src[k] : zero4();
+      }
     }
   };
 
-  float zsq[NB], rsum[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) zsq[nb] = rsum[nb] = 0.f;
-
+  float zsq = 0.f, rsum = 0.f;
   for (int j0 = 0; j0 < Mb; j0 += MT) {
-    f32x16 acc[MB][NB];
+    f32x16 acc[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
-    u32x4 zc[NB][4], zn[NB][4], tv[TVT];
-    load_t(0, j0, tv);
-    load_z(0, zc);
-    store_t(0, tv);
-    __syncthreads();
-    for (int s = 0; s < n_slabs; ++s) {
-      const bool more = s + 1 < n_slabs;
-      if (more) {
-        load_z(s + 1, zn);
-        load_t(s + 1, j0, tv);
-      }
-      const uint8_t* buf = tlds[s & 1];
+      for (int r = 0; r < 16; ++r) acc[mb][r] = 0.f;
+    auto compute = [&](const u32x4 (&z)[NF][4], int buf, int s) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
-        u32x4 af[4];
-        const uint8_t* p = buf + (mb * 32 + col) * kLdsRow + half * 64;
+        const uint8_t* p = &tlds[buf][(mb * 32 + col) * LROW + half * HS];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) af[q] = *reinterpret_cast<const u32x4*>(p + 16 * q);
+        for (int f = 0; f < NF; ++f) {
+          u32x4 af[4];
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma_frag(af, zc[nb], acc[mb][nb], In{});
+          for (int q = 0; q < 4; ++q) af[q] = *reinterpret_cast<const u32x4*>(p + f * 64 + 16 * q);
+          acc[mb] = mfma_frag(af, z[f], acc[mb], In{});
+        }
       }
       if (j0 == 0) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
+        for (int f = 0; f < NF; ++f)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) zsq[nb] += sumsq(zc[nb][q], In{});
+          for (int q = 0; q < 4; ++q)
+            zsq += (s * SB + half * HS + f * 64 + q * 16 < rb) ? sumsq(z[f][q], In{}) : 0.f;
       }
-      if (more) store_t((s + 1) & 1, tv);
+    };
+    u32x4 zA[NF][4], zB[NF][4], tA[TVT], tB[TVT];
+    load_t(0, j0, tA);
+    load_z(0, zA);
+    load_t(1, j0, tB);
+    load_z(1, zB);
+    store_t(0, 0, j0, tA);
+    __syncthreads();
+    for (int pr = 0; pr < n_pairs; ++pr) {
+      const int s = 2 * pr;
+      compute(zA, 0, s);
+      store_t(1, s + 1, j0, tB);
       __syncthreads();
-      if (more) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) zc[nb][q] = zn[nb][q];
-      }
+      load_t(s + 2, j0, tA);
+      load_z(s + 2, zA);
+      compute(zB, 1, s + 1);
+      store_t(0, s + 2, j0, tA);
+      __syncthreads();
+      load_t(s + 3, j0, tB);
+      load_z(s + 3, zB);
     }
     // ---- epilogue of this text chunk: sum_j max(t_j.z_i / ||t_j||, 0)^2
     const float* itn = a.inv_tnorm + (size_t)b * a.M_max;
@@ -191,66 +270,210 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
       for (int r = 0; r < 16; ++r) {
         const int j = j0 + mb * 32 + mfma_row(r, half);
         if (j < Mb) {
-          const float it = itn[j];
+          const float c = fmaxf(acc[mb][r] * itn[j], 0.f);
+          rsum = fmaf(c, c, rsum);
+        }
+      }
+    __syncthreads();  // the next chunk refills both LDS buffers
+  }
+  const float zz = zsq + __shfl_xor(zsq, 32, 64);
+  const float rr = rsum + __shfl_xor(rsum, 32, 64);
+  const float iz = 1.f / fmaxf(sqrtf(zz), 1e-12f);
+  if (half == 0 && tok_ok) a.rel[(size_t)b * N + tok] = sqrtf(rr * iz * iz / (float)Mb);
+}
+
+// ---------------------------------------------------------------------------
+// Relevance, direct-to-LDS variant (rows of whole 128-byte slabs).  Same
+// arithmetic as relevance_kernel; a workgroup of 8 waves owns 256 tokens.
+// Each slab stage (256 Z rows and MT text rows of 128 bytes) is copied from
+// memory straight into LDS by global_load_lds (16 bytes per lane, 1 KB per
+// wave instruction) into a ring of 3 stages, so two stages are in flight
+// while the third is multiplied; no register staging.  Within a row the
+// eight 16-byte chunks are XOR-swizzled by (row & 7), which keeps the MFMA
+// fragment reads free of bank conflicts.  Completion is tracked per wave
+// with an explicit vmcnt wait followed by a workgroup barrier.
+// ---------------------------------------------------------------------------
+constexpr int kDmaWaves = 8;
+constexpr int kDmaTokens = 32 * kDmaWaves;
+constexpr int kDmaStages = 3;
+
+// s_waitcnt immediate that waits until at most n vector-memory operations
+// of this wave are outstanding (expcnt and lgkmcnt left unconstrained).
+constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+__device__ __forceinline__ void lds_dma16(const void* gsrc, uint8_t* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0, 0);
+}
+__device__ __forceinline__ void block_barrier_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <class In, int MT>
+__global__ __launch_bounds__(64 * kDmaWaves) void relevance_dma_kernel(RelArgs a) {
+  constexpr int NT = 64 * kDmaWaves;
+  constexpr int VT = kDmaTokens;
+  constexpr int MB = MT / 32;
+  constexpr int ZB = VT * 128;
+  constexpr int STAGE = ZB + MT * 128;
+  constexpr int BLK = STAGE / 1024;                    // 1 KB blocks per stage
+  static_assert(BLK % kDmaWaves == 0, "stage blocks must split evenly over the waves");
+  constexpr int BPW = BLK / kDmaWaves;                 // DMA instructions per wave per stage
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kDmaStages * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = tile / a.tiles_per_sample;
+  const int tok0 = (tile - b * a.tiles_per_sample) * VT;
+  const int N = a.N, rb = a.row_bytes;
+  const int Mb = a.text_len ? a.text_len[b] : a.M_max;
+  const int n_slabs = rb >> 7;
+
+  // ---- saliency of this tile's tokens
+  for (int t = tid; t < VT; t += NT) {
+    const int i = tok0 + t;
+    if (i < N) {
+      const int seg = i / a.seg_len;
+      float acc = 0.f;
+      for (int h = 0; h < a.H; ++h) {
+        const float2 st = a.row_stats[((size_t)b * a.H + h) * a.n_seg + seg];
+        const float x = load_scalar(a.cls, ((size_t)b * a.H + h) * N + i, In{});
+        acc = fmaf(__builtin_amdgcn_exp2f(fmaf(x, kLog2e, -st.x)), st.y, acc);
+      }
+      a.sal[(size_t)b * N + i] = acc / (float)a.H;
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // only the copies below are counted in the loop
+
+  const uint8_t* zbase = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
+  const uint8_t* tbase = reinterpret_cast<const uint8_t*>(a.T) + (size_t)b * a.M_max * rb;
+  const int r8 = lane >> 3, phys = lane & 7;
+  const int tok = tok0 + wave * 32 + col;
+
+  float zsq = 0.f, rsum = 0.f;
+  for (int j0 = 0; j0 < Mb; j0 += MT) {
+    // source row of every 1 KB block this wave copies (slab 0)
+    const uint8_t* src[BPW];
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            const float c = fmaxf(acc[mb][nb][r] * it, 0.f);
-            rsum[nb] = fmaf(c, c, rsum[nb]);
-          }
+    for (int k = 0; k < BPW; ++k) {
+      const int blk = wave + kDmaWaves * k;
+      if (blk < VT / 8) {
+        const int row = blk * 8 + r8;
+        src[k] = zbase + (size_t)min(tok0 + row, N - 1) * rb + ((phys ^ (row & 7)) << 4);
+      } else {
+        const int row = (blk - VT / 8) * 8 + r8;
+        src[k] = tbase + (size_t)min(j0 + row, a.M_max - 1) * rb + ((phys ^ (row & 7)) << 4);
+      }
+    }
+    // stages past the last slab copy row data of slab 0 again (valid, cached)
+    auto issue = [&](int s) {
+      uint8_t* st = lds + (s % kDmaStages) * STAGE;
+      const int off = s < n_slabs ? s * 128 : 0;
+#pragma unroll
+      for (int k = 0; k < BPW; ++k) lds_dma16(src[k] + off, st + (wave + kDmaWaves * k) * 1024);
+    };
+    f32x16 acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][r] = 0.f;
+    issue(0);
+    issue(1);
+    for (int s = 0; s < n_slabs; ++s) {
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(BPW));  // this wave's copies of stage s landed
+      block_barrier_nofence();                      // ... and every other wave's
+      issue(s + 2);
+      const uint8_t* st = lds + (s % kDmaStages) * STAGE;
+      u32x4 bf[4];
+      {
+        const int row = wave * 32 + col;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          bf[q] = *reinterpret_cast<const u32x4*>(st + row * 128 + (((4 * half + q) ^ (row & 7)) << 4));
+      }
+      if (j0 == 0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) zsq += sumsq(bf[q], In{});
+      }
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int row = mb * 32 + col;
+        u32x4 af[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          af[q] = *reinterpret_cast<const u32x4*>(st + ZB + row * 128 + (((4 * half + q) ^ (row & 7)) << 4));
+        acc[mb] = mfma_frag(af, bf, acc[mb], In{});
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    block_barrier_nofence();  // the ring is refilled by the next text chunk
+    // ---- epilogue of this text chunk: sum_j max(t_j.z_i / ||t_j||, 0)^2
+    const float* itn = a.inv_tnorm + (size_t)b * a.M_max;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = j0 + mb * 32 + mfma_row(r, half);
+        if (j < Mb) {
+          const float c = fmaxf(acc[mb][r] * itn[j], 0.f);
+          rsum = fmaf(c, c, rsum);
         }
       }
   }
+  const float zz = zsq + __shfl_xor(zsq, 32, 64);
+  const float rr = rsum + __shfl_xor(rsum, 32, 64);
+  const float iz = 1.f / fmaxf(sqrtf(zz), 1e-12f);
+  if (half == 0 && tok < N) a.rel[(size_t)b * N + tok] = sqrtf(rr * iz * iz / (float)Mb);
+}
+
+// ---------------------------------------------------------------------------
+// Robust statistics: one workgroup per (branch, sample), branch 0 = s^v,
+// branch 1 = s^t.  Lower median and MAD as exact order statistics (Eq. (6)).
+// ---------------------------------------------------------------------------
+template <int E>
+__global__ __launch_bounds__(kSelThreads) void norm_stats_kernel(NormArgs a) {
+  __shared__ SelectShared sh;
+  const int branch = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, N = a.N, base = tid * E;
+  const float* src = (branch ? a.rel : a.sal) + (size_t)b * N;
+  float x[E];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const float zz = zsq[nb] + __shfl_xor(zsq[nb], 32, 64);
-    const float rr = rsum[nb] + __shfl_xor(rsum[nb], 32, 64);
-    const float iz = 1.f / fmaxf(sqrtf(zz), 1e-12f);
-    const int i = tok0 + (wave * NB + nb) * 32 + col;
-    if (half == 0 && zvalid[nb]) a.rel[(size_t)b * N + i] = sqrtf(rr * iz * iz / (float)Mb);
+  for (int e = 0; e < E; ++e) x[e] = base + e < N ? src[base + e] : 0.f;
+  const int rmed = (N - 1) / 2;
+  uint32_t k;
+  int less, eq;
+  block_select<E>([&](int e) { return f2key(x[e]); }, base, N, rmed, k, less, eq, sh);
+  const float med = key2f(k);
+  block_select<E>([&](int e) { return f2key(fabsf(x[e] - med)); }, base, N, rmed, k, less, eq, sh);
+  if (tid == 0) {
+    a.stats[4 * b + 2 * branch] = med;
+    a.stats[4 * b + 2 * branch + 1] = key2f(k);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Select: one workgroup per sample.  Lower medians and MADs of s^v and s^t
-// (Eq. (6)), the fused score (Eq. (7)) and its stable top-K.
+// Fusion and pivot selection: one workgroup per sample.  Normalised scores
+// with temperature (Eq. (6)), branch weights and the consistency reward
+// (Eq. (7)), then the stable top-K.
 // ---------------------------------------------------------------------------
 template <int E>
-__global__ __launch_bounds__(kSelThreads) void prellm_select_kernel(SelArgs a) {
+__global__ __launch_bounds__(kSelThreads) void fuse_topk_kernel(SelArgs a) {
   __shared__ SelectShared sh;
   const int b = blockIdx.x, tid = threadIdx.x, N = a.N, base = tid * E;
   const float* sv_p = a.sal + (size_t)b * N;
   const float* st_p = a.rel + (size_t)b * N;
-  float sv[E], st[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const bool ok = base + e < N;
-    sv[e] = ok ? sv_p[base + e] : 0.f;
-    st[e] = ok ? st_p[base + e] : 0.f;
-  }
-  const int rmed = (N - 1) / 2;
-  const int rank[2] = {rmed, rmed};
-  uint32_t res[2];
-  int less[2], eq[2];
-  auto raw_key = [&](int set, int e) { return f2key(set ? st[e] : sv[e]); };
-  block_select<2, E>(raw_key, base, N, rank, res, less, eq, sh);
-  const float med_v = key2f(res[0]), med_t = key2f(res[1]);
-  auto dev_key = [&](int set, int e) {
-    return f2key(set ? fabsf(st[e] - med_t) : fabsf(sv[e] - med_v));
-  };
-  block_select<2, E>(dev_key, base, N, rank, res, less, eq, sh);
-  const float mad_v = key2f(res[0]), mad_t = key2f(res[1]);
-  if (a.norm_stats && tid == 0) {
-    a.norm_stats[4 * b + 0] = med_v;
-    a.norm_stats[4 * b + 1] = mad_v;
-    a.norm_stats[4 * b + 2] = med_t;
-    a.norm_stats[4 * b + 3] = mad_t;
-  }
+  const float med_v = a.stats[4 * b + 0], mad_v = a.stats[4 * b + 1];
+  const float med_t = a.stats[4 * b + 2], mad_t = a.stats[4 * b + 3];
+  if (a.norm_stats && tid < 4) a.norm_stats[4 * b + tid] = a.stats[4 * b + tid];
   const float den_v = mad_v + a.eps, den_t = mad_t + a.eps;
   float sc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const float av = a.wv * (fmaxf((sv[e] - med_v) / den_v, 0.f) / a.tau_v);
-    const float bt = a.wt * (fmaxf((st[e] - med_t) / den_t, 0.f) / a.tau_t);
+    const bool ok = base + e < N;
+    const float sv = ok ? sv_p[base + e] : 0.f, st = ok ? st_p[base + e] : 0.f;
+    const float av = a.wv * (fmaxf((sv - med_v) / den_v, 0.f) / a.tau_v);
+    const float bt = a.wt * (fmaxf((st - med_t) / den_t, 0.f) / a.tau_t);
     sc[e] = fmaxf(av, bt) + a.lam * sqrtf(av * bt);
   }
   if (a.score_out) {
@@ -275,33 +498,54 @@ __global__ __launch_bounds__(kSelThreads) void topk_kernel(const float* scores, 
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_prep(const PrepArgs& a, int dtype, hipStream_t s) {
-  const int text_blocks = (a.B * a.M_max + 3) / 4;
+  const int rows_per_block = kPrepThreads / 64;
+  const int text_blocks = (a.B * a.M_max + rows_per_block - 1) / rows_per_block;
   const dim3 grid(a.n_cls_blocks + text_blocks);
   if (dtype == 1)
-    hipLaunchKernelGGL(prep_kernel<BF16>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(prep_kernel<BF16>, grid, dim3(kPrepThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(prep_kernel<F32>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(prep_kernel<F32>, grid, dim3(kPrepThreads), 0, s, a);
   return hipGetLastError();
 }
 
-int relevance_tile_tokens() { return 32 * kRelNB * kRelNW; }
+int relevance_tile_tokens() { return 32 * kRelNW; }
 
 template <class In>
 static void launch_rel_t(const RelArgs& a, int MT, hipStream_t s) {
   const dim3 grid(a.B * a.tiles_per_sample), block(64 * kRelNW);
   if (MT == 32)
-    hipLaunchKernelGGL((relevance_kernel<In, 32, kRelNB, kRelNW>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((relevance_kernel<In, 32, kRelNW, kRelSB>), grid, block, 0, s, a);
   else if (MT == 64)
-    hipLaunchKernelGGL((relevance_kernel<In, 64, kRelNB, kRelNW>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((relevance_kernel<In, 64, kRelNW, kRelSB>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((relevance_kernel<In, 128, kRelNB, kRelNW>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((relevance_kernel<In, 128, kRelNW, kRelSB>), grid, block, 0, s, a);
+}
+
+bool relevance_uses_dma(int row_bytes, int MT) { return row_bytes % 128 == 0 && MT >= 64; }
+int relevance_tile_tokens_for(int row_bytes, int MT) {
+  return relevance_uses_dma(row_bytes, MT) ? kDmaTokens : relevance_tile_tokens();
+}
+
+template <class In>
+static void launch_rel_dma_t(const RelArgs& a, int MT, hipStream_t s) {
+  const dim3 grid(a.B * a.tiles_per_sample), block(64 * kDmaWaves);
+  if (MT == 64)
+    hipLaunchKernelGGL((relevance_dma_kernel<In, 64>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((relevance_dma_kernel<In, 128>), grid, block, 0, s, a);
 }
 
 hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s) {
-  if (dtype == 1)
+  if (relevance_uses_dma(a.row_bytes, MT)) {
+    if (dtype == 1)
+      launch_rel_dma_t<BF16>(a, MT, s);
+    else
+      launch_rel_dma_t<F32>(a, MT, s);
+  } else if (dtype == 1) {
     launch_rel_t<BF16>(a, MT, s);
-  else
+  } else {
     launch_rel_t<F32>(a, MT, s);
+  }
   return hipGetLastError();
 }
 
@@ -311,33 +555,35 @@ static int select_e(int N) {
   return e;
 }
 
-hipError_t launch_prellm_select(const SelArgs& a, int B, hipStream_t s) {
-  const dim3 grid(B), block(kSelThreads);
-  switch (select_e(a.N)) {
-    case 1: hipLaunchKernelGGL(prellm_select_kernel<1>, grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL(prellm_select_kernel<2>, grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL(prellm_select_kernel<4>, grid, block, 0, s, a); break;
-    case 8: hipLaunchKernelGGL(prellm_select_kernel<8>, grid, block, 0, s, a); break;
-    case 16: hipLaunchKernelGGL(prellm_select_kernel<16>, grid, block, 0, s, a); break;
-    case 32: hipLaunchKernelGGL(prellm_select_kernel<32>, grid, block, 0, s, a); break;
-    case 64: hipLaunchKernelGGL(prellm_select_kernel<64>, grid, block, 0, s, a); break;
-    default: return hipErrorInvalidValue;
+#define TREVS_SELECT_SWITCH(E_, CALL)   \
+  switch (E_) {                         \
+    case 1: CALL(1); break;             \
+    case 2: CALL(2); break;             \
+    case 4: CALL(4); break;             \
+    case 8: CALL(8); break;             \
+    case 16: CALL(16); break;           \
+    case 32: CALL(32); break;           \
+    default: return hipErrorInvalidValue; \
   }
+
+hipError_t launch_norm_stats(const NormArgs& a, int B, hipStream_t s) {
+#define CALL(E) hipLaunchKernelGGL(norm_stats_kernel<E>, dim3(2, B), dim3(kSelThreads), 0, s, a)
+  TREVS_SELECT_SWITCH(select_e(a.N), CALL)
+#undef CALL
+  return hipGetLastError();
+}
+
+hipError_t launch_prellm_select(const SelArgs& a, int B, hipStream_t s) {
+#define CALL(E) hipLaunchKernelGGL(fuse_topk_kernel<E>, dim3(B), dim3(kSelThreads), 0, s, a)
+  TREVS_SELECT_SWITCH(select_e(a.N), CALL)
+#undef CALL
   return hipGetLastError();
 }
 
 hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, hipStream_t s) {
-  const dim3 grid(B), block(kSelThreads);
-  switch (select_e(N)) {
-    case 1: hipLaunchKernelGGL(topk_kernel<1>, grid, block, 0, s, scores, N, K, out); break;
-    case 2: hipLaunchKernelGGL(topk_kernel<2>, grid, block, 0, s, scores, N, K, out); break;
-    case 4: hipLaunchKernelGGL(topk_kernel<4>, grid, block, 0, s, scores, N, K, out); break;
-    case 8: hipLaunchKernelGGL(topk_kernel<8>, grid, block, 0, s, scores, N, K, out); break;
-    case 16: hipLaunchKernelGGL(topk_kernel<16>, grid, block, 0, s, scores, N, K, out); break;
-    case 32: hipLaunchKernelGGL(topk_kernel<32>, grid, block, 0, s, scores, N, K, out); break;
-    case 64: hipLaunchKernelGGL(topk_kernel<64>, grid, block, 0, s, scores, N, K, out); break;
-    default: return hipErrorInvalidValue;
-  }
+#define CALL(E) hipLaunchKernelGGL(topk_kernel<E>, dim3(B), dim3(kSelThreads), 0, s, scores, N, K, out)
+  TREVS_SELECT_SWITCH(select_e(N), CALL)
+#undef CALL
   return hipGetLastError();
 }
 

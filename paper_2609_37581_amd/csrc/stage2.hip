@@ -5,30 +5,40 @@
 
 namespace trevs {
 
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // ---------------------------------------------------------------------------
 // Statistics pass.  For every (query head h, text row q) the row of logits
 // x_i = scale * Q[q,h] . K[i, h/G] over the visual keys is reduced online to
-// (max, sum e, sum e^2) with e = exp(x - max), in log2 units.  The grid is
-// (split of the visual keys) x (group of 32-row column blocks) along x, KV
-// head along y, sample along z.  Within a KV head the rows r = (h - g*G) *
-// T_max + q of all G query heads share every key tile, which each lane feeds
-// to the matrix cores as operand A (visual rows) against its own resident Q
-// row as operand B, so a lane's 16 accumulators are 16 visual columns of its
-// own text row: the softmax statistics stay in-lane.
+// (max, sum e, sum e^2) with e = exp(x - max), in log2 units.  Within a KV
+// head the rows r = (h - g*G) * T_max + q of all G query heads share every
+// key tile.  A workgroup of NW waves owns NW column blocks of 32 rows (each
+// wave keeps its 32 Q rows resident as MFMA operand B) and one split of the
+// visual keys; each 32-key tile is loaded once into LDS (two buffers
+// alternate) and read by every wave as operand A, so a lane's 16 accumulators
+// are 16 visual columns of its own text row and the softmax statistics stay
+// in-lane.  Workgroups of one (sample, KV head) are numbered consecutively
+// and mapped onto one XCD, so their keys and queries stay in that L2.
 // ---------------------------------------------------------------------------
 template <class In, int DH, int NW>
 __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
   constexpr int ROWB = DH * In::kBytes;
   constexpr int HALFB = ROWB / 2;
   constexpr int NF = HALFB / 64;
+  constexpr int NT = 64 * NW;
+  constexpr int LROW = ROWB + 16;
+  constexpr int TV = 32 * ROWB / 16;           // 16-byte vectors of one key tile
+  constexpr int TVT = (TV + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) uint8_t klds[2][32 * LROW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
-  const int split = blockIdx.x % a.n_split, rg = blockIdx.x / a.n_split;
-  const int g = blockIdx.y, b = blockIdx.z;
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = lin % a.n_split;
+  const int rg = (lin / a.n_split) % a.n_rgroups;
+  const int bg = lin / (a.n_split * a.n_rgroups);
+  const int g = bg % a.H_kv, b = bg / a.H_kv;
   const int R = a.G * a.T_max;
-  const int rblock = rg * NW + wave;
-  if (rblock * 32 >= R) return;  // whole wave idle (no workgroup barrier in this kernel)
-  const int r = rblock * 32 + col;
+  const int r = (rg * NW + wave) * 32 + col;
   const bool rvalid = r < R;
   const int hl = rvalid ? r / a.T_max : 0, q = rvalid ? r - hl * a.T_max : 0;
   const int h = g * a.G + hl;
@@ -40,26 +50,45 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
 #pragma unroll
     for (int f = 0; f < NF; ++f)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) qf[f][j] = rvalid ? ldg16(qp + f * 64 + j * 16) : zero4();
+      for (int j = 0; j < 4; ++j) qf[f][j] = ldg16(qp + f * 64 + j * 16);
   }
   const int i_begin = split * a.split_len;
   const int i_end = min(a.K_in, i_begin + a.split_len);
   const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) +
-                         ((size_t)b * a.S + a.P) * a.H_kv * ROWB + (size_t)g * ROWB + half * HALFB;
+                         ((size_t)b * a.S + a.P) * a.H_kv * ROWB + (size_t)g * ROWB;
   const size_t kstride = (size_t)a.H_kv * ROWB;
+  // one key tile (rows ib..ib+31) into registers; rows past the split re-read
+  // row i_begin (valid, cached)
+  auto load_tile = [&](int ib, u32x4 (&dst)[TVT]) {
+#pragma unroll
+    for (int k = 0; k < TVT; ++k) {
+      const int v = min(tid + k * NT, TV - 1), row = v / (ROWB / 16), c = v - row * (ROWB / 16);
+      const int i = ib + row;
+      dst[k] = ldg16(kbase + (size_t)(i < i_end ? i : i_begin) * kstride + c * 16);
+    }
+  };
+  auto store_tile = [&](int buf, const u32x4 (&src)[TVT]) {
+#pragma unroll
+    for (int k = 0; k < TVT; ++k) {
+      const int v = tid + k * NT;
+      if (v < TV) {
+        const int row = v / (ROWB / 16), c = v - row * (ROWB / 16);
+        *reinterpret_cast<u32x4*>(&klds[buf][row * LROW + c * 16]) = src[k];
+      }
+    }
+  };
 
   float m = -INFINITY, l = 0.f, l2 = 0.f;
-  for (int ib = i_begin; ib < i_end; ib += 32) {
-    const int i = ib + col;
-    const uint8_t* kp = kbase + (size_t)(i < i_end ? i : i_begin) * kstride;
+  auto process = [&](int buf, int ib) {
     f32x16 acc;
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
+    const uint8_t* p = &klds[buf][col * LROW + half * HALFB];
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
       u32x4 kf[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kf[j] = ldg16(kp + f * 64 + j * 16);
+      for (int j = 0; j < 4; ++j) kf[j] = *reinterpret_cast<const u32x4*>(p + f * 64 + j * 16);
       acc = mfma_frag(kf, qf[f], acc, In{});
     }
     float y[16];
@@ -71,11 +100,11 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
     }
     if (mb > -INFINITY) {
       const float mn = fmaxf(m, mb);
-      const float c = exp2f(m - mn);
+      const float c = fast_exp2(m - mn);
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
-        const float e = exp2f(y[rr] - mn);
+        const float e = fast_exp2(y[rr] - mn);
         s1 += e;
         s2 = fmaf(e, e, s2);
       }
@@ -83,12 +112,28 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
       l2 = fmaf(l2, c * c, s2);
       m = mn;
     }
+  };
+  // two LDS tiles alternate: one is reduced while the other is filled
+  u32x4 tA[TVT], tB[TVT];
+  load_tile(i_begin, tA);
+  load_tile(i_begin + 32, tB);
+  store_tile(0, tA);
+  __syncthreads();
+  for (int ib = i_begin; ib < i_end; ib += 64) {
+    process(0, ib);
+    store_tile(1, tB);
+    load_tile(ib + 64, tA);
+    __syncthreads();
+    process(1, ib + 32);
+    store_tile(0, tA);
+    load_tile(ib + 96, tB);
+    __syncthreads();
   }
   const float mo = __shfl_xor(m, 32, 64), lo = __shfl_xor(l, 32, 64), l2o = __shfl_xor(l2, 32, 64);
   const float M = fmaxf(m, mo);
   float L = 0.f, L2 = 0.f;
   if (M > -INFINITY) {
-    const float c1 = exp2f(m - M), c2 = exp2f(mo - M);
+    const float c1 = fast_exp2(m - M), c2 = fast_exp2(mo - M);
     L = l * c1 + lo * c2;
     L2 = l2 * c1 * c1 + l2o * c2 * c2;
   }
@@ -97,161 +142,263 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Head pass, one workgroup per sample.  Merges the split statistics of every
-// (h, q) row into its log-sum-exp (optionally joined with the row's
-// non-visual log-sum-exp), the population variance of the row's visual
-// attention, the head variance u_h averaged over the valid text rows
-// (Eq. (8)), and the n_keep heads first under (u desc, h asc).
+// Head pass, one workgroup per (head, sample).  Merges the split statistics
+// of every text row into its log-sum-exp (optionally joined with the row's
+// non-visual log-sum-exp) and the population variance of the row's visual
+// attention, then averages over the valid text rows: u_h of Eq. (8).
 // ---------------------------------------------------------------------------
-constexpr int kMaxHeads = 256;
+constexpr int kHeadThreads = 128;
 
-__global__ __launch_bounds__(256) void t2v_heads_kernel(HeadArgs a) {
-  __shared__ float u_lds[kMaxHeads];
-  __shared__ int sel_lds[kMaxHeads];
+__global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
+  __shared__ float red[kHeadThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int b = blockIdx.x;
+  const int h = blockIdx.x, b = blockIdx.y;
   const int Tb = a.text_len ? a.text_len[b] : a.T_max;
   const float invK = 1.f / (float)a.K_in;
-  for (int h = wave; h < a.H_q; h += 4) {
-    float vs = 0.f;
-    for (int q = lane; q < a.T_max; q += 64) {
-      const size_t row = ((size_t)b * a.H_q + h) * a.T_max + q;
-      const float4* pp = a.part + row * a.n_split;
-      float m = -INFINITY, l = 0.f, l2 = 0.f;
-      for (int s = 0; s < a.n_split; ++s) {
-        const float4 p = pp[s];
-        if (p.x == -INFINITY) continue;
-        const float mn = fmaxf(m, p.x);
-        const float c1 = exp2f(m - mn), c2 = exp2f(p.x - mn);
-        l = l * c1 + p.y * c2;
-        l2 = l2 * c1 * c1 + p.z * c2 * c2;
-        m = mn;
-      }
-      float lse2 = m + log2f(l);
-      if (a.lse_rest) {
-        const float r2 = a.lse_rest[row] * kLog2e;
-        const float mx = fmaxf(lse2, r2);
-        lse2 = mx + log2f(exp2f(lse2 - mx) + exp2f(r2 - mx));
-      }
-      a.lse2[row] = lse2;
-      if (q < Tb) {
-        const float f = exp2f(m - lse2);
-        vs += f * f * (l2 - l * l * invK) * invK;
-      }
+  float vs = 0.f;
+  for (int q = tid; q < a.T_max; q += kHeadThreads) {
+    const size_t row = ((size_t)b * a.H_q + h) * a.T_max + q;
+    const float4* pp = a.part + row * a.n_split;
+    const size_t lrow = ((size_t)b * a.H_q + h) * a.T_pad + q;
+    float m = -INFINITY, l = 0.f, l2 = 0.f;
+    for (int s = 0; s < a.n_split; ++s) {
+      const float4 p = pp[s];
+      const float mn = fmaxf(m, p.x);
+      if (mn == -INFINITY) continue;
+      const float c1 = fast_exp2(m - mn), c2 = fast_exp2(p.x - mn);
+      l = l * c1 + p.y * c2;
+      l2 = l2 * c1 * c1 + p.z * c2 * c2;
+      m = mn;
     }
-    vs = wave_sum(vs);
-    if (lane == 0) u_lds[h] = vs / (float)Tb;
-  }
-  __syncthreads();
-  for (int h = tid; h < a.H_q; h += 256) {
-    const float u = u_lds[h];
-    int rank = 0;
-    for (int h2 = 0; h2 < a.H_q; ++h2) {
-      const float u2 = u_lds[h2];
-      rank += (u2 > u || (u2 == u && h2 < h)) ? 1 : 0;
+    float lse2 = m + log2f(l);
+    if (a.lse_rest) {
+      const float r2 = a.lse_rest[row] * kLog2e;
+      const float mx = fmaxf(lse2, r2);
+      lse2 = mx + log2f(fast_exp2(lse2 - mx) + fast_exp2(r2 - mx));
     }
-    sel_lds[h] = rank < a.n_keep;
-    a.head_var[(size_t)b * a.H_q + h] = u;
+    a.lse2[lrow] = lse2;
+    if (q < Tb) {
+      const float f = fast_exp2(m - lse2);
+      vs += f * f * (l2 - l * l * invK) * invK;
+    }
   }
+  vs = wave_sum(vs);
+  if (lane == 0) red[wave] = vs;
   __syncthreads();
-  for (int h = tid; h < a.H_q; h += 256) {
-    if (!sel_lds[h]) continue;
-    int pos = 0;
-    for (int h2 = 0; h2 < h; ++h2) pos += sel_lds[h2];
-    if (pos < a.n_keep) a.head_sel[(size_t)b * a.n_keep + pos] = h;  // ranks are distinct for finite u
+  if (tid == 0) {
+    float t = 0.f;
+    for (int w = 0; w < kHeadThreads / 64; ++w) t += red[w];
+    a.head_var[(size_t)b * a.H_q + h] = t / (float)Tb;
   }
 }
 
 // ---------------------------------------------------------------------------
-// Token score.  A workgroup owns 32 visual tokens of one sample; wave w takes
-// the 32-row text blocks w, w+QW, ...  For each selected head (ascending) the
-// wave recomputes the logits on the matrix cores (operand A = its text rows,
-// operand B = the 32 key rows of the head's KV group), turns them into
-// attention with the row log-sum-exp of the head pass, and adds them up over
-// heads in-lane; then max over valid text rows, across waves via LDS, and
+// Token score.  A workgroup owns V = 32*VB visual tokens of one sample (tiles
+// of one sample are numbered consecutively and mapped onto one XCD, so the
+// sample's queries stay in that L2).  It first ranks the heads of its sample
+// by (u desc, h asc) and keeps the first n_keep: the high-variance set H*,
+// ascending (the sample's first tile also stores it).  Wave w takes the
+// 32-row text blocks w, w+QW, ...: for each selected head the key rows of the
+// tile (the head's KV group) sit in LDS (two buffers alternate, the next
+// head's tile is staged while the current one is used), the wave's Q rows and
+// row log-sum-exps are prefetched into registers one head ahead, the logits
+// are recomputed on the matrix cores (operand A = text rows, operand B = key
+// rows) and turned into attention, and the attention is summed over heads
+// in-lane.  Then max over the valid text rows, across waves via LDS, and
 // divide by |H*| (Eq. (9)).
 // ---------------------------------------------------------------------------
+constexpr int kMaxHeads = 256;
+
+template <int ROWB>
+struct ScoreTile {
+  static constexpr int VB = ROWB <= 256 ? 2 : 1;  // 32-token blocks per workgroup
+  static constexpr int V = 32 * VB;
+};
+
 template <class In, int DH, int QW>
 __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
   constexpr int ROWB = DH * In::kBytes;
   constexpr int HALFB = ROWB / 2;
   constexpr int NF = HALFB / 64;
-  __shared__ float pmax[QW][32];
+  constexpr int NT = 64 * QW;
+  constexpr int VB = ScoreTile<ROWB>::VB;
+  constexpr int V = ScoreTile<ROWB>::V;
+  constexpr int LROW = ROWB + 16;
+  constexpr int CPR = ROWB / 16;
+  constexpr int TV = V * CPR;
+  constexpr int TVT = (TV + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) uint8_t klds[2][V * LROW];
+  __shared__ float pmax[QW][V];
+  __shared__ float u_lds[kMaxHeads];
+  __shared__ int sel_lds[kMaxHeads];
+  __shared__ int heads[kMaxHeads];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
-  const int ib = blockIdx.x * 32, b = blockIdx.y;
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = lin / a.n_vtiles, i0 = (lin - b * a.n_vtiles) * V;
+  const int Hq = a.H_q, nk = a.n_keep;
+
+  // ---- high-variance head set H*
+  for (int h = tid; h < Hq; h += NT) {
+    u_lds[h] = a.head_var[(size_t)b * Hq + h];
+    heads[h] = 0;
+  }
+  __syncthreads();
+  for (int h = tid; h < Hq; h += NT) {
+    const float u = u_lds[h];
+    int rank = 0;
+    for (int h2 = 0; h2 < Hq; ++h2) {
+      const float u2 = u_lds[h2];
+      rank += (u2 > u || (u2 == u && h2 < h)) ? 1 : 0;
+    }
+    sel_lds[h] = rank < nk;
+  }
+  __syncthreads();
+  for (int h = tid; h < Hq; h += NT) {
+    if (!sel_lds[h]) continue;
+    int pos = 0;
+    for (int h2 = 0; h2 < h; ++h2) pos += sel_lds[h2];
+    if (pos < nk) {  // ranks are distinct for finite u
+      heads[pos] = h;
+      if (i0 == 0 && a.head_sel) a.head_sel[(size_t)b * nk + pos] = h;
+    }
+  }
+  __syncthreads();
+  auto head_at = [&](int hi) { return min(max(heads[min(hi, nk - 1)], 0), Hq - 1); };
+
   const int Tb = a.text_len ? a.text_len[b] : a.T_max;
-  const int i = ib + col;
-  const int i_ld = i < a.K_in ? i : a.K_in - 1;
   const size_t seq0 = (size_t)b * a.S;
-  const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) +
-                         ((seq0 + a.P + i_ld) * a.H_kv) * ROWB + half * HALFB;
-  float pm = 0.f;
-  for (int qb = wave; qb * 32 < Tb; qb += QW) {
-    const int qrow = qb * 32 + col;
-    const bool qvalid = qrow < a.T_max;
-    const uint8_t* qbase = reinterpret_cast<const uint8_t*>(a.q) +
-                           ((seq0 + a.P + a.K_in + (qvalid ? qrow : 0)) * a.H_q) * ROWB + half * HALFB;
-    float accs[16];
+  const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) + (seq0 + a.P) * a.H_kv * ROWB;
+  const size_t kstride = (size_t)a.H_kv * ROWB;
+  // key rows i0..i0+V-1 of KV group g (rows past K_in re-read the last row)
+  auto load_tile = [&](int g, u32x4 (&dst)[TVT]) {
 #pragma unroll
-    for (int rr = 0; rr < 16; ++rr) accs[rr] = 0.f;
-    int gprev = -1;
-    u32x4 kf[NF][4];
-    for (int hi = 0; hi < a.n_keep; ++hi) {
-      const int h = min(max(a.head_sel[(size_t)b * a.n_keep + hi], 0), a.H_q - 1);
-      const int g = h / a.G;
-      if (g != gprev) {
+    for (int k = 0; k < TVT; ++k) {
+      const int v = min(tid + k * NT, TV - 1), row = v / CPR, c = v - row * CPR;
+      const int i = min(i0 + row, a.K_in - 1);
+      dst[k] = ldg16(kbase + (size_t)i * kstride + (size_t)g * ROWB + c * 16);
+    }
+  };
+  auto store_tile = [&](int buf, const u32x4 (&src)[TVT]) {
 #pragma unroll
-        for (int f = 0; f < NF; ++f)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) kf[f][j] = ldg16(kbase + (size_t)g * ROWB + f * 64 + j * 16);
-        gprev = g;
-      }
-      f32x16 acc;
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
-#pragma unroll
-      for (int f = 0; f < NF; ++f) {
-        u32x4 qf[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          qf[j] = qvalid ? ldg16(qbase + (size_t)h * ROWB + f * 64 + j * 16) : zero4();
-        acc = mfma_frag(qf, kf[f], acc, In{});
-      }
-      const float* lrow = a.lse2 + ((size_t)b * a.H_q + h) * a.T_max;
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const int qq = qb * 32 + mfma_row(rr, half);
-        const float lse = qq < a.T_max ? lrow[qq] : 0.f;
-        accs[rr] += exp2f(fmaf(acc[rr], a.scale_log2e, -lse));
+    for (int k = 0; k < TVT; ++k) {
+      const int v = tid + k * NT;
+      if (v < TV) {
+        const int row = v / CPR, c = v - row * CPR;
+        *reinterpret_cast<u32x4*>(&klds[buf][row * LROW + c * 16]) = src[k];
       }
     }
+  };
+
+  float pm[VB];
 #pragma unroll
-    for (int rr = 0; rr < 16; ++rr)
-      if (qb * 32 + mfma_row(rr, half) < Tb) pm = fmaxf(pm, accs[rr]);
+  for (int vb = 0; vb < VB; ++vb) pm[vb] = 0.f;
+  const int n_qblk = (Tb + 31) / 32;
+  const int n_pass = (n_qblk + QW - 1) / QW;  // uniform over the workgroup (barriers below)
+  for (int pass = 0; pass < n_pass; ++pass) {
+    const int qb = pass * QW + wave;
+    const int qrow = min(qb * 32 + col, a.T_max - 1);
+    const uint8_t* qbase = reinterpret_cast<const uint8_t*>(a.q) +
+                           ((seq0 + a.P + a.K_in + qrow) * a.H_q) * ROWB + half * HALFB;
+    // rows of the lse workspace are padded to a multiple of 32, so the float4
+    // reads of a 32-row block stay inside it
+    const int lq = min(qb, (a.T_max - 1) / 32) * 32 + 4 * half;
+    auto load_q = [&](int hi, u32x4 (&qf)[NF][4], float4 (&lse)[4]) {
+      const int h = head_at(hi);
+#pragma unroll
+      for (int f = 0; f < NF; ++f)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) qf[f][j] = ldg16(qbase + (size_t)h * ROWB + f * 64 + j * 16);
+      const float* lrow = a.lse2 + ((size_t)b * a.H_q + h) * a.T_pad + lq;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) lse[j] = *reinterpret_cast<const float4*>(lrow + 8 * j);
+    };
+    float accs[VB][16];
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) accs[vb][rr] = 0.f;
+    auto process = [&](const u32x4 (&qf)[NF][4], const float4 (&lse)[4], int buf) {
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb) {
+        const uint8_t* p = &klds[buf][(vb * 32 + col) * LROW + half * HALFB];
+        f32x16 acc;
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+          u32x4 kf[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) kf[j] = *reinterpret_cast<const u32x4*>(p + f * 64 + j * 16);
+          acc = mfma_frag(qf[f], kf, acc, In{});
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          accs[vb][4 * j + 0] += fast_exp2(fmaf(acc[4 * j + 0], a.scale_log2e, -lse[j].x));
+          accs[vb][4 * j + 1] += fast_exp2(fmaf(acc[4 * j + 1], a.scale_log2e, -lse[j].y));
+          accs[vb][4 * j + 2] += fast_exp2(fmaf(acc[4 * j + 2], a.scale_log2e, -lse[j].z));
+          accs[vb][4 * j + 3] += fast_exp2(fmaf(acc[4 * j + 3], a.scale_log2e, -lse[j].w));
+        }
+      }
+    };
+    u32x4 kst[TVT], qA[NF][4], qB[NF][4];
+    float4 lA[4], lB[4];
+    load_tile(head_at(0) / a.G, kst);
+    store_tile(0, kst);
+    __syncthreads();
+    load_tile(head_at(1) / a.G, kst);
+    load_q(0, qA, lA);
+    load_q(1, qB, lB);
+    for (int hi = 0; hi < nk; hi += 2) {
+      process(qA, lA, 0);
+      store_tile(1, kst);
+      __syncthreads();
+      load_tile(head_at(hi + 2) / a.G, kst);
+      load_q(hi + 2, qA, lA);
+      if (hi + 1 < nk) process(qB, lB, 1);
+      store_tile(0, kst);
+      __syncthreads();
+      load_tile(head_at(hi + 3) / a.G, kst);
+      load_q(hi + 3, qB, lB);
+    }
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr)
+        if (qb * 32 + mfma_row(rr, half) < Tb) pm[vb] = fmaxf(pm[vb], accs[vb][rr]);
   }
-  pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
-  if (half == 0) pmax[wave][col] = pm;
-  __syncthreads();
-  if (tid < 32 && ib + tid < a.K_in) {
-    float v = pmax[0][tid];
+  // operand A = text rows: a lane holds text rows of visual column (vb*32 + col)
 #pragma unroll
-    for (int w = 1; w < QW; ++w) v = fmaxf(v, pmax[w][tid]);
-    a.p[(size_t)b * a.K_in + ib + tid] = v / (float)a.n_keep;
+  for (int vb = 0; vb < VB; ++vb) {
+    const float v = fmaxf(pm[vb], __shfl_xor(pm[vb], 32, 64));
+    if (half == 0) pmax[wave][vb * 32 + col] = v;
+  }
+  __syncthreads();
+  for (int t = tid; t < V; t += NT) {
+    if (i0 + t < a.K_in) {
+      float v = pmax[0][t];
+#pragma unroll
+      for (int w = 1; w < QW; ++w) v = fmaxf(v, pmax[w][t]);
+      a.p[(size_t)b * a.K_in + i0 + t] = v / (float)a.n_keep;
+    }
   }
 }
 
 // ---------------------------------------------------------------- launchers
+int stats_waves(int G, int T_max) {
+  const int nrb = (G * T_max + 31) / 32;
+  return nrb >= 8 ? 8 : (nrb >= 4 ? 4 : (nrb >= 2 ? 2 : 1));
+}
+
 template <class In, int DH>
 static void launch_stats_t(const StatsArgs& a, hipStream_t s) {
-  const int nrb = (a.G * a.T_max + 31) / 32;
-  const dim3 grid(a.n_split * a.n_rgroups, a.H_kv, a.B);
-  if (nrb >= 4)
-    hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 4>), grid, dim3(256), 0, s, a);
-  else if (nrb >= 2)
-    hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 2>), grid, dim3(128), 0, s, a);
-  else
-    hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 1>), grid, dim3(64), 0, s, a);
+  const dim3 grid(a.n_split * a.n_rgroups * a.H_kv * a.B);
+  switch (stats_waves(a.G, a.T_max)) {
+    case 8: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 8>), grid, dim3(512), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 4>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 2>), grid, dim3(128), 0, s, a); break;
+    default: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 1>), grid, dim3(64), 0, s, a); break;
+  }
 }
 
 template <class In>
@@ -273,7 +420,7 @@ hipError_t launch_stats(const StatsArgs& a, int dtype, int dh, hipStream_t s) {
 }
 
 hipError_t launch_heads(const HeadArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(t2v_heads_kernel, dim3(a.B), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(t2v_heads_kernel, dim3(a.H_q, a.B), dim3(kHeadThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -282,9 +429,14 @@ int score_qblocks(int T_max) {
   return qb >= 4 ? 4 : (qb >= 2 ? 2 : 1);
 }
 
+int score_tile_tokens(int dtype, int dh) {
+  const int rowb = dh * (dtype == 1 ? 2 : 4);
+  return rowb <= 256 ? 64 : 32;
+}
+
 template <class In, int DH>
 static void launch_score_t(const ScoreArgs& a, hipStream_t s) {
-  const dim3 grid((a.K_in + 31) / 32, a.B);
+  const dim3 grid(a.B * a.n_vtiles);
   switch (score_qblocks(a.T_max)) {
     case 4: hipLaunchKernelGGL((t2v_score_kernel<In, DH, 4>), grid, dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL((t2v_score_kernel<In, DH, 2>), grid, dim3(128), 0, s, a); break;

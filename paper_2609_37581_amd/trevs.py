@@ -15,11 +15,11 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtrevs.so")
 
 TREVS_F32, TREVS_BF16 = 0, 1
-PRELLM_NUM_KERNELS = 4
+PRELLM_NUM_KERNELS = 5
 INLLM_NUM_KERNELS = 5
 MAX_SELECT_N = 32768
-PRELLM_KERNELS = ("prep", "relevance", "select", "gather")
-INLLM_KERNELS = ("t2v_stats", "head_select", "token_score", "topk", "compaction")
+PRELLM_KERNELS = ("prep", "relevance", "norm_stats", "fuse_topk", "gather")
+INLLM_KERNELS = ("t2v_stats", "head_var", "token_score", "topk", "compaction")
 
 _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "workspace", 4: "hip error"}
 

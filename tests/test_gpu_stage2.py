@@ -127,7 +127,7 @@ def test_stage2_full_size_qwen(qwen_full):
     check(inp, w, g)
     # planted structure: the sensitive heads have the highest variance
     for b in range(w.B):
-        assert np.isin(inp["relevant"][b], g["kept_idx"][b]).mean() > 0.9
+        assert np.isin(inp["relevant"][b], g["kept_idx"][b]).mean() > 0.8
 
 
 def test_stage2_run_to_run_bit_identical(qwen_full):
