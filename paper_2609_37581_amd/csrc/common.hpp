@@ -94,33 +94,52 @@ __device__ __forceinline__ void stg16_stream(void* p, u32x4 v) {
 __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 
 // ---------------------------------------------------------------- reductions
+// Wave-wide reductions and scans on DPP lane moves (no LDS traffic): four
+// row_shr steps combine the 16 lanes of a row, then row_bcast:15 and
+// row_bcast:31 carry across rows; lane 63 ends with the full result.
+namespace dpp {
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ int mov(int old, int v) {
+  return __builtin_amdgcn_update_dpp(old, v, CTRL, ROW_MASK, 0xf, false);
+}
+constexpr int kShr1 = 0x111, kShr2 = 0x112, kShr4 = 0x114, kShr8 = 0x118;
+constexpr int kBcast15 = 0x142, kBcast31 = 0x143;
+}  // namespace dpp
+
+template <class Op>
+__device__ __forceinline__ int wave_reduce_bits(int v, int identity, Op op) {
+  v = op(v, dpp::mov<dpp::kShr1>(identity, v));
+  v = op(v, dpp::mov<dpp::kShr2>(identity, v));
+  v = op(v, dpp::mov<dpp::kShr4>(identity, v));
+  v = op(v, dpp::mov<dpp::kShr8>(identity, v));
+  v = op(v, dpp::mov<dpp::kBcast15, 0xa>(identity, v));
+  v = op(v, dpp::mov<dpp::kBcast31, 0xc>(identity, v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  return __int_as_float(wave_reduce_bits(__float_as_int(v), 0, [](int a, int b) {
+    return __float_as_int(__int_as_float(a) + __int_as_float(b));
+  }));
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+  return __int_as_float(wave_reduce_bits(__float_as_int(v), __float_as_int(-INFINITY), [](int a, int b) {
+    return __float_as_int(fmaxf(__int_as_float(a), __int_as_float(b)));
+  }));
 }
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, o, kWave));
-  return v;
+  return (uint32_t)wave_reduce_bits((int)v, -1, [](int a, int b) { return (int)min((uint32_t)a, (uint32_t)b); });
 }
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
-  return v;
+  return (uint32_t)wave_reduce_bits((int)v, 0, [](int a, int b) { return (int)max((uint32_t)a, (uint32_t)b); });
 }
-// Inclusive prefix sum across the wave.
-__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int t = __shfl_up(v, o, kWave);
-    if (lane >= o) v += t;
-  }
+// Inclusive prefix sum across the wave (lane argument kept for call sites).
+__device__ __forceinline__ int wave_incl_scan(int v, int /*lane*/) {
+  v += dpp::mov<dpp::kShr1>(0, v);
+  v += dpp::mov<dpp::kShr2>(0, v);
+  v += dpp::mov<dpp::kShr4>(0, v);
+  v += dpp::mov<dpp::kShr8>(0, v);
+  v += dpp::mov<dpp::kBcast15, 0xa>(0, v);
+  v += dpp::mov<dpp::kBcast31, 0xc>(0, v);
   return v;
 }
 

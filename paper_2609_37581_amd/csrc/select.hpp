@@ -1,6 +1,6 @@
 // Workgroup-wide exact order statistics and stable top-K.  One workgroup of
-// 1024 threads ranks one vector; thread t owns the E consecutive elements
-// [t*E, t*E + E), so a workgroup prefix sum walks the elements in index order.
+// 1024 threads ranks one vector; thread t owns elements t, t + 1024, ...,
+// (element e*1024 + t is its e-th), so loads and stores are coalesced.
 #pragma once
 
 #include "common.hpp"
@@ -14,9 +14,12 @@ constexpr int kFirstBins = 1 << kFirstBits;
 constexpr int kLaterBits = 8;                 // digit width of the candidate passes
 constexpr int kCandCap = 4096;                // candidates kept in LDS after the first pass
 
+constexpr int kMaxE = 32;                     // elements per thread (N <= 32768)
+
 struct SelectShared {
   uint32_t hist[kFirstBins];
   uint32_t cand[kCandCap];
+  int wcnt[kMaxE * kSelWaves];                // per (element round, wave) counts
   uint32_t mn[kSelWaves];
   uint32_t mx[kSelWaves];
   int wave_tot[kSelWaves];
@@ -31,35 +34,17 @@ __device__ __forceinline__ int block_excl_scan(int v, SelectShared& sh, int& tot
   const int inc = wave_incl_scan(v, lane);
   if (lane == kWave - 1) sh.wave_tot[wave] = inc;
   __syncthreads();
-  if (wave == 0) {
-    const int w = lane < kSelWaves ? sh.wave_tot[lane] : 0;
-    const int wi = wave_incl_scan(w, lane);
-    if (lane < kSelWaves) sh.wave_excl[lane] = wi - w;
-    if (lane == kSelWaves - 1) sh.total = wi;
-  }
-  __syncthreads();
-  total = sh.total;
-  const int r = sh.wave_excl[wave] + inc - v;
-  __syncthreads();
-  return r;
+  // every wave scans the (few) wave totals itself
+  const int wt = lane < kSelWaves ? sh.wave_tot[lane] : 0;
+  const int wi = wave_incl_scan(wt, lane);
+  const int before = __builtin_amdgcn_readlane(wi - wt, wave);
+  total = __builtin_amdgcn_readlane(wi, kSelWaves - 1);
+  __syncthreads();  // sh.wave_tot is rewritten by the next call
+  return before + inc - v;
 }
 
-// Histogram increment.  The lanes that share the first active lane's digit
-// are counted with one atomic (values cluster, e.g. exact zeros, which would
-// otherwise serialise on one LDS address); the others add one each.  Must be
-// called by every lane of the wave.
-__device__ __forceinline__ void hist_add(uint32_t* hist, bool act, uint32_t digit) {
-  const unsigned long long am = __ballot(act);
-  if (am == 0ull) return;
-  const int leader = __ffsll((long long)am) - 1;
-  const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)digit, leader);
-  const unsigned long long same = __ballot(act && digit == d0);
-  if ((int)(threadIdx.x & (kWave - 1)) == leader) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
-  if (act && digit != d0) atomicAdd(&hist[digit], 1u);
-}
-
-// Finds the bin holding rank krem in hist[0, nbins): every thread owns two
-// bins, a workgroup scan orders them.  Result in sh.res_*.
+// Finds the bin holding rank krem in hist[0, nbins) (nbins <= 2 * 1024):
+// thread t owns bins 2t and 2t+1, a workgroup scan orders them.
 __device__ __forceinline__ void block_find_bin(int nbins, int krem, SelectShared& sh) {
   const int t = threadIdx.x;
   const int c0 = 2 * t < nbins ? (int)sh.hist[2 * t] : 0;
@@ -104,41 +89,67 @@ __device__ __forceinline__ void wave0_find_bin(int krem, SelectShared& sh) {
   __syncthreads();
 }
 
+// Histogram pass over this thread's elements: keys equal to the set minimum
+// `kmin` (often a large tie, e.g. exact zeros) are counted with one ballot per
+// wave and added once; every other key adds one to its digit's bin.
+template <int E, class KeyF, class Match>
+__device__ __forceinline__ void hist_pass(KeyF keyf, Match match, int N, uint32_t kmin, int shift,
+                                          uint32_t dmask, SelectShared& sh) {
+  const int lane = threadIdx.x & (kWave - 1);
+  int nmin = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const uint32_t k = keyf(e);
+    const bool act = e * kSelThreads + (int)threadIdx.x < N && match(k);
+    const bool is_min = act && k == kmin;
+    nmin += __popcll(__ballot(is_min));
+    if (act && !is_min) atomicAdd(&sh.hist[(k >> shift) & dmask], 1u);
+  }
+  if (lane == 0 && nmin) atomicAdd(&sh.hist[(kmin >> shift) & dmask], (uint32_t)nmin);
+}
+
 // Exact rank selection on uint32 keys.  keyf(e) yields the key of this
 // thread's element e (recomputed on demand, not held).  Returns the key of
 // ascending 0-based rank `rank` among the N valid keys, with the number of
-// keys strictly below it (less) and equal to it (eq).
-//   1. min and max; the bits above their highest differing bit are common.
+// keys strictly below it (less) and equal to it (eq).  If have_range, kmin and
+// kmax are the minimum and maximum key (else they are computed).
+//   1. the bits above the highest bit where min and max differ are common;
 //   2. one pass over all elements on the next (up to) 11 bits;
-//   3. the elements in the chosen bin are compacted into LDS (if they fit)
-//      and the remaining bits are resolved 8 at a time over them alone;
-//      otherwise the remaining passes scan all elements.
+//   3. the keys in the chosen bin are appended to LDS (if they fit) and the
+//      remaining bits are resolved 8 at a time over them alone; otherwise the
+//      remaining passes scan all elements.
 template <int E, class KeyF>
-__device__ void block_select(KeyF keyf, int base, int N, int rank, uint32_t& res, int& less,
-                             int& eq, SelectShared& sh) {
+__device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& less, int& eq,
+                             SelectShared& sh, bool have_range = false, uint32_t kmin = 0u,
+                             uint32_t kmax = 0u) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  uint32_t mn = 0xffffffffu, mx = 0u;
+  auto valid = [&](int e) { return e * kSelThreads + tid < N; };
+  uint32_t a = kmin, z = kmax;
+  if (!have_range) {
+    uint32_t mn = 0xffffffffu, mx = 0u;
 #pragma unroll
-  for (int e = 0; e < E; ++e)
-    if (base + e < N) {
-      const uint32_t k = keyf(e);
-      mn = min(mn, k);
-      mx = max(mx, k);
+    for (int e = 0; e < E; ++e)
+      if (valid(e)) {
+        const uint32_t k = keyf(e);
+        mn = min(mn, k);
+        mx = max(mx, k);
+      }
+    mn = wave_min_u32(mn);
+    mx = wave_max_u32(mx);
+    if (lane == 0) {
+      sh.mn[wave] = mn;
+      sh.mx[wave] = mx;
     }
-  mn = wave_min_u32(mn);
-  mx = wave_max_u32(mx);
-  if (lane == 0) {
-    sh.mn[wave] = mn;
-    sh.mx[wave] = mx;
-  }
-  __syncthreads();
-  uint32_t a = 0xffffffffu, z = 0u;
+    __syncthreads();
+    a = 0xffffffffu;
+    z = 0u;
 #pragma unroll
-  for (int w = 0; w < kSelWaves; ++w) {
-    a = min(a, sh.mn[w]);
-    z = max(z, sh.mx[w]);
+    for (int w = 0; w < kSelWaves; ++w) {
+      a = min(a, sh.mn[w]);
+      z = max(z, sh.mx[w]);
+    }
+    __syncthreads();  // sh.mn / sh.mx are rewritten by the next call
   }
-  __syncthreads();  // sh.mn / sh.mx are rewritten by the next call
   const uint32_t diff = a ^ z;
   less = 0;
   if (diff == 0u) {
@@ -149,17 +160,18 @@ __device__ void block_select(KeyF keyf, int base, int N, int rank, uint32_t& res
   int nb = 32 - __clz(diff);
   uint32_t prefix = (uint32_t)(((uint64_t)a >> nb) << nb);
   int krem = rank;
+  auto under_prefix = [&](uint32_t k) { return ((uint64_t)k >> nb) == ((uint64_t)prefix >> nb); };
 
   // ---- first pass: every element shares the prefix above bit nb
   {
     const int db = min(kFirstBits, nb), shift = nb - db;
-    const uint32_t dmask = (1u << db) - 1u;
-    for (int i = tid; i < (1 << db); i += kSelThreads) sh.hist[i] = 0u;
+    const int nbins = 1 << db;
+    for (int i = tid; i < nbins; i += kSelThreads) sh.hist[i] = 0u;
+    if (tid == 0) sh.total = 0;
     __syncthreads();
-#pragma unroll
-    for (int e = 0; e < E; ++e) hist_add(sh.hist, base + e < N, (keyf(e) >> shift) & dmask);
+    hist_pass<E>(keyf, [](uint32_t) { return true; }, N, a, shift, (1u << db) - 1u, sh);
     __syncthreads();
-    block_find_bin(1 << db, krem, sh);
+    block_find_bin(nbins, krem, sh);
     prefix |= sh.res_digit << shift;
     krem -= (int)sh.res_before;
     less += (int)sh.res_before;
@@ -172,18 +184,24 @@ __device__ void block_select(KeyF keyf, int base, int N, int rank, uint32_t& res
   }
   const int ncand = eq;
   if (ncand <= kCandCap) {
-    // ---- compact the candidates (keys sharing the prefix above bit nb)
-    int mine = 0;
+    // ---- append the candidates (keys sharing the prefix above bit nb);
+    // their order does not matter for a rank selection.  One LDS atomic per
+    // wave reserves room for all of the wave's candidates.
+    int wn = 0;
 #pragma unroll
-    for (int e = 0; e < E; ++e)
-      mine += (base + e < N && ((uint64_t)keyf(e) >> nb) == ((uint64_t)prefix >> nb)) ? 1 : 0;
-    int tot;
-    int off = block_excl_scan(mine, sh, tot);
+    for (int e = 0; e < E; ++e) wn += __popcll(__ballot(valid(e) && under_prefix(keyf(e))));
+    int wbase = 0;
+    if (lane == 0 && wn) wbase = atomicAdd(&sh.total, wn);
+    wbase = __builtin_amdgcn_readfirstlane(wbase);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const uint32_t k = keyf(e);
-      if (base + e < N && ((uint64_t)k >> nb) == ((uint64_t)prefix >> nb) && off < kCandCap)
-        sh.cand[off++] = k;
+      const bool m = valid(e) && under_prefix(k);
+      const unsigned long long bal = __ballot(m);
+      const int pos = wbase + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+      if (m && pos < kCandCap) sh.cand[pos] = k;
+      wbase += __popcll(bal);
     }
     __syncthreads();
     const int rounds = (ncand + kSelThreads - 1) / kSelThreads;
@@ -195,8 +213,7 @@ __device__ void block_select(KeyF keyf, int base, int N, int rank, uint32_t& res
       for (int r = 0; r < rounds; ++r) {
         const int c = r * kSelThreads + tid;
         const uint32_t k = c < ncand ? sh.cand[c] : 0u;
-        const bool act = c < ncand && ((uint64_t)k >> nb) == ((uint64_t)prefix >> nb);
-        hist_add(sh.hist, act, (k >> shift) & dmask);
+        if (c < ncand && under_prefix(k)) atomicAdd(&sh.hist[(k >> shift) & dmask], 1u);
       }
       __syncthreads();
       wave0_find_bin(krem, sh);
@@ -211,15 +228,9 @@ __device__ void block_select(KeyF keyf, int base, int N, int rank, uint32_t& res
     // ---- many keys share the first digit: resolve the rest over all elements
     while (nb > 0) {
       const int db = min(kLaterBits, nb), shift = nb - db;
-      const uint32_t dmask = (1u << db) - 1u;
       if (tid < (1 << kLaterBits)) sh.hist[tid] = 0u;
       __syncthreads();
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const uint32_t k = keyf(e);
-        const bool act = base + e < N && ((uint64_t)k >> nb) == ((uint64_t)prefix >> nb);
-        hist_add(sh.hist, act, (k >> shift) & dmask);
-      }
+      hist_pass<E>(keyf, under_prefix, N, a, shift, (1u << db) - 1u, sh);
       __syncthreads();
       wave0_find_bin(krem, sh);
       prefix |= sh.res_digit << shift;
@@ -233,38 +244,75 @@ __device__ void block_select(KeyF keyf, int base, int N, int rank, uint32_t& res
   res = prefix;
 }
 
+// Exclusive prefix sums of sh.wcnt[0, n) in place (n <= kMaxE * kSelWaves),
+// by wave 0; entries are ordered (element round, wave), which is index order.
+__device__ __forceinline__ void wcnt_scan(int n, SelectShared& sh) {
+  __syncthreads();
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    const int per = (n + kWave - 1) / kWave;
+    int* c = sh.wcnt + lane * per;
+    int lsum = 0;
+    for (int j = 0; j < per; ++j)
+      if (lane * per + j < n) lsum += c[j];
+    int run = wave_incl_scan(lsum, lane) - lsum;
+    for (int j = 0; j < per; ++j)
+      if (lane * per + j < n) {
+        const int v = c[j];
+        c[j] = run;
+        run += v;
+      }
+  }
+  __syncthreads();
+}
+
 // Stable top-K: keep every element whose score is above the K-th largest and
 // the lowest-index elements equal to it, and write the kept indices in
 // ascending order to out[0..K).
 template <int E>
-__device__ void block_topk_write(const float (&sc)[E], int base, int N, int K, int32_t* out,
+__device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* out,
                                  SelectShared& sh) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   auto keyf = [&](int e) { return f2key(sc[e]); };
+  auto valid = [&](int e) { return e * kSelThreads + tid < N; };
   uint32_t thr;
   int less, eq;
-  block_select<E>(keyf, base, N, N - K, thr, less, eq, sh);
+  block_select<E>(keyf, N, N - K, thr, less, eq, sh);
   const int need_eq = K - (N - less - eq);
-  int my_eq = 0;
-#pragma unroll
-  for (int e = 0; e < E; ++e) my_eq += (base + e < N && keyf(e) == thr) ? 1 : 0;
-  int tot;
-  int run = block_excl_scan(my_eq, sh, tot);
-  uint32_t keep_mask = 0u;
-  int my_keep = 0;
+  auto lanes_below = [&](unsigned long long bal) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+  };
+  // rank of every tie among the ties, in index order (ballots are recomputed
+  // after each scan rather than held)
+  auto is_eq = [&](int e) { return valid(e) && keyf(e) == thr; };
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const bool valid = base + e < N;
-    const uint32_t k = keyf(e);
-    const bool is_eq = valid && k == thr;
-    const bool keep = valid && (k > thr || (is_eq && run < need_eq));
-    run += is_eq ? 1 : 0;
-    keep_mask |= keep ? (1u << e) : 0u;
-    my_keep += keep ? 1 : 0;
+    const unsigned long long bal = __ballot(is_eq(e));
+    if (lane == 0) sh.wcnt[e * kSelWaves + wave] = __popcll(bal);
   }
-  int pos = block_excl_scan(my_keep, sh, tot);
+  wcnt_scan(E * kSelWaves, sh);
+  uint32_t keep_mask = 0u;
 #pragma unroll
-  for (int e = 0; e < E; ++e)
-    if (((keep_mask >> e) & 1u) && pos < K) out[pos++] = base + e;  // exactly K kept; bound guards memory
+  for (int e = 0; e < E; ++e) {
+    const bool eqe = is_eq(e);
+    const int eq_rank = sh.wcnt[e * kSelWaves + wave] + lanes_below(__ballot(eqe));
+    const bool keep = valid(e) && (keyf(e) > thr || (eqe && eq_rank < need_eq));
+    keep_mask |= keep ? (1u << e) : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const unsigned long long bal = __ballot((keep_mask >> e) & 1u);
+    if (lane == 0) sh.wcnt[e * kSelWaves + wave] = __popcll(bal);
+  }
+  wcnt_scan(E * kSelWaves, sh);
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const bool kp = (keep_mask >> e) & 1u;
+    const int pos = sh.wcnt[e * kSelWaves + wave] + lanes_below(__ballot(kp));
+    if (kp && pos < K) out[pos] = e * kSelThreads + tid;  // exactly K kept; the bound guards memory
+  }
 }
 
 }  // namespace trevs

@@ -435,17 +435,47 @@ __global__ __launch_bounds__(64 * kDmaWaves) void relevance_dma_kernel(RelArgs a
 template <int E>
 __global__ __launch_bounds__(kSelThreads) void norm_stats_kernel(NormArgs a) {
   __shared__ SelectShared sh;
-  const int branch = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, N = a.N, base = tid * E;
+  __shared__ float red_lo[kSelWaves], red_hi[kSelWaves];
+  const int branch = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, N = a.N;
   const float* src = (branch ? a.rel : a.sal) + (size_t)b * N;
   float x[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) x[e] = base + e < N ? src[base + e] : 0.f;
+  for (int e = 0; e < E; ++e) {
+    const int i = e * kSelThreads + tid;
+    x[e] = i < N ? src[i] : 0.f;
+  }
+  // min and max of the scores, then the median
+  float lo = INFINITY, hi = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (e * kSelThreads + tid < N) {
+      lo = fminf(lo, x[e]);
+      hi = fmaxf(hi, x[e]);
+    }
+  lo = -wave_max(-lo);
+  hi = wave_max(hi);
+  if ((tid & 63) == 0) {
+    red_lo[tid >> 6] = lo;
+    red_hi[tid >> 6] = hi;
+  }
+  __syncthreads();
+  lo = INFINITY;
+  hi = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    lo = fminf(lo, red_lo[w]);
+    hi = fmaxf(hi, red_hi[w]);
+  }
   const int rmed = (N - 1) / 2;
   uint32_t k;
   int less, eq;
-  block_select<E>([&](int e) { return f2key(x[e]); }, base, N, rmed, k, less, eq, sh);
+  block_select<E>([&](int e) { return f2key(x[e]); }, N, rmed, k, less, eq, sh, true, f2key(lo),
+                  f2key(hi));
   const float med = key2f(k);
-  block_select<E>([&](int e) { return f2key(fabsf(x[e] - med)); }, base, N, rmed, k, less, eq, sh);
+  // the deviations |x - Med| range from 0 (the median itself) to the larger
+  // distance of the extremes, computed with the same fp32 operation
+  block_select<E>([&](int e) { return f2key(fabsf(x[e] - med)); }, N, rmed, k, less, eq, sh, true,
+                  f2key(0.f), f2key(fmaxf(fabsf(lo - med), fabsf(hi - med))));
   if (tid == 0) {
     a.stats[4 * b + 2 * branch] = med;
     a.stats[4 * b + 2 * branch + 1] = key2f(k);
@@ -460,7 +490,7 @@ __global__ __launch_bounds__(kSelThreads) void norm_stats_kernel(NormArgs a) {
 template <int E>
 __global__ __launch_bounds__(kSelThreads) void fuse_topk_kernel(SelArgs a) {
   __shared__ SelectShared sh;
-  const int b = blockIdx.x, tid = threadIdx.x, N = a.N, base = tid * E;
+  const int b = blockIdx.x, tid = threadIdx.x, N = a.N;
   const float* sv_p = a.sal + (size_t)b * N;
   const float* st_p = a.rel + (size_t)b * N;
   const float med_v = a.stats[4 * b + 0], mad_v = a.stats[4 * b + 1];
@@ -470,30 +500,30 @@ __global__ __launch_bounds__(kSelThreads) void fuse_topk_kernel(SelArgs a) {
   float sc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const bool ok = base + e < N;
-    const float sv = ok ? sv_p[base + e] : 0.f, st = ok ? st_p[base + e] : 0.f;
+    const int i = e * kSelThreads + tid;
+    const bool ok = i < N;
+    const float sv = ok ? sv_p[i] : 0.f, st = ok ? st_p[i] : 0.f;
     const float av = a.wv * (fmaxf((sv - med_v) / den_v, 0.f) / a.tau_v);
     const float bt = a.wt * (fmaxf((st - med_t) / den_t, 0.f) / a.tau_t);
     sc[e] = fmaxf(av, bt) + a.lam * sqrtf(av * bt);
+    if (a.score_out && ok) a.score_out[(size_t)b * N + i] = sc[e];
   }
-  if (a.score_out) {
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-      if (base + e < N) a.score_out[(size_t)b * N + base + e] = sc[e];
-  }
-  block_topk_write<E>(sc, base, N, a.K, a.kept_idx + (size_t)b * a.K, sh);
+  block_topk_write<E>(sc, N, a.K, a.kept_idx + (size_t)b * a.K, sh);
 }
 
 template <int E>
 __global__ __launch_bounds__(kSelThreads) void topk_kernel(const float* scores, int N, int K,
                                                            int32_t* out) {
   __shared__ SelectShared sh;
-  const int b = blockIdx.x, base = threadIdx.x * E;
+  const int b = blockIdx.x, tid = threadIdx.x;
   const float* p = scores + (size_t)b * N;
   float sc[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) sc[e] = base + e < N ? p[base + e] : 0.f;
-  block_topk_write<E>(sc, base, N, K, out + (size_t)b * K, sh);
+  for (int e = 0; e < E; ++e) {
+    const int i = e * kSelThreads + tid;
+    sc[e] = i < N ? p[i] : 0.f;
+  }
+  block_topk_write<E>(sc, N, K, out + (size_t)b * K, sh);
 }
 
 // ---------------------------------------------------------------- launchers
