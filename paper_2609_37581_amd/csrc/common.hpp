@@ -54,25 +54,27 @@ __device__ __forceinline__ float sumsq(u32x4 v, F32) {
   return s;
 }
 
-// C[32x32] += A[32 x k] * B[k x 32] over one 64-byte fragment per lane.
-// Lane l supplies row (l % 32) of A and column (l % 32) of B; its half
-// (l / 32) selects which 64-byte half of a 128-byte row chunk it carries.
-// A and B lanes carry the same k values element for element, so any
-// assignment of k to (half, element) that both operands share contracts
-// correctly.  Output layout: lane l holds column (l % 32), register r holds
-// row 8*(r/4) + 4*(l/32) + (r%4).
-__device__ __forceinline__ f32x16 mfma_frag(const u32x4 (&a)[4], const u32x4 (&b)[4], f32x16 c,
+// C[32x32] += A[32 x k] * B[k x 32] over one fragment of NQ 16-byte chunks
+// per lane.  Lane l supplies row (l % 32) of A and column (l % 32) of B; its
+// half (l / 32) selects which half of a row slab it carries.  A and B lanes
+// carry the same k values element for element, so any assignment of k to
+// (half, chunk, element) that both operands share contracts correctly.
+// Output layout: lane l holds column (l % 32), register r holds row
+// 8*(r/4) + 4*(l/32) + (r%4).
+template <int NQ>
+__device__ __forceinline__ f32x16 mfma_frag(const u32x4 (&a)[NQ], const u32x4 (&b)[NQ], f32x16 c,
                                             BF16) {
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
+  for (int s = 0; s < NQ; ++s)
     c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[s]),
                                                 __builtin_bit_cast(bf16x8, b[s]), c, 0, 0, 0);
   return c;
 }
-__device__ __forceinline__ f32x16 mfma_frag(const u32x4 (&a)[4], const u32x4 (&b)[4], f32x16 c,
+template <int NQ>
+__device__ __forceinline__ f32x16 mfma_frag(const u32x4 (&a)[NQ], const u32x4 (&b)[NQ], f32x16 c,
                                             F32) {
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
+  for (int s = 0; s < NQ; ++s)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[s][j]), __uint_as_float(b[s][j]),

@@ -117,6 +117,37 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
   if (lane == 0) a.inv_tnorm[r] = inv;
 }
 
+// Saliency (Eq. (2)-(3)) of the tokens [tok0, tok0 + VT) of sample b: the
+// head mean of each [CLS] logit's softmax within its segment, from the
+// per-(head, segment) max and 1/sum written by prep_kernel.  The head loop
+// is unrolled by 8 with all loads of a group issued before the first use,
+// so a tile pays about H/8 memory round trips instead of H.
+template <class In>
+__device__ __forceinline__ void tile_saliency(const RelArgs& a, int b, int tok0, int VT, int NT, int tid) {
+  const int N = a.N, H = a.H;
+  for (int t = tid; t < VT; t += NT) {
+    const int i = tok0 + t;
+    if (i < N) {
+      const int seg = i / a.seg_len;
+      float acc = 0.f;
+      for (int h0 = 0; h0 < H; h0 += 8) {
+        float2 st[8];
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int h = min(h0 + u, H - 1);
+          st[u] = a.row_stats[((size_t)b * H + h) * a.n_seg + seg];
+          x[u] = load_scalar(a.cls, ((size_t)b * H + h) * N + i, In{});
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (h0 + u < H) acc = fmaf(__builtin_amdgcn_exp2f(fmaf(x[u], kLog2e, -st[u].x)), st[u].y, acc);
+      }
+      a.sal[(size_t)b * N + i] = acc / (float)H;
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Relevance: one pass over the visual features Z.  A workgroup owns 32*NW
 // consecutive visual tokens of one sample; each wave owns 32 of them and
@@ -163,20 +194,7 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
   const int n_slabs = (rb + SB - 1) / SB;
   const int n_pairs = (n_slabs + 1) / 2;
 
-  // ---- saliency of this tile's tokens
-  for (int t = tid; t < VT; t += NT) {
-    const int i = tok0 + t;
-    if (i < N) {
-      const int seg = i / a.seg_len;
-      float acc = 0.f;
-      for (int h = 0; h < a.H; ++h) {
-        const float2 st = a.row_stats[((size_t)b * a.H + h) * a.n_seg + seg];
-        const float x = load_scalar(a.cls, ((size_t)b * a.H + h) * N + i, In{});
-        acc = fmaf(__builtin_amdgcn_exp2f(fmaf(x, kLog2e, -st.x)), st.y, acc);
-      }
-      a.sal[(size_t)b * N + i] = acc / (float)a.H;
-    }
-  }
+  tile_saliency<In>(a, b, tok0, VT, NT, tid);
 
   const int tok = tok0 + wave * 32 + col;
   const bool tok_ok = tok < N;
@@ -283,23 +301,40 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Relevance, direct-to-LDS variant (rows of whole 128-byte slabs).  Same
-// arithmetic as relevance_kernel; a workgroup of 8 waves owns 256 tokens.
-// Each slab stage (256 Z rows and MT text rows of 128 bytes) is copied from
-// memory straight into LDS by global_load_lds (16 bytes per lane, 1 KB per
-// wave instruction) into a ring of 3 stages, so two stages are in flight
-// while the third is multiplied; no register staging.  Within a row the
-// eight 16-byte chunks are XOR-swizzled by (row & 7), which keeps the MFMA
-// fragment reads free of bank conflicts.  Completion is tracked per wave
-// with an explicit vmcnt wait followed by a workgroup barrier.
+// Relevance, direct-to-LDS variant (rows made of whole slabs of SLAB bytes,
+// text tile of 64 or 128 rows).  Same arithmetic as relevance_kernel; a
+// workgroup of 8 waves owns 256 tokens.  Each stage (the SLAB-byte slab of
+// the 256 Z rows and of the MT text rows) is copied from memory straight into
+// LDS by global_load_lds (16 bytes per lane, 1 KB per wave instruction,
+// whole slabs of consecutive rows, so every instruction reads full lines)
+// into a ring of RING stages: RING - 1 stages are in flight while one is
+// multiplied.  Every wave issues the same number of copies per stage, so one
+// explicit vmcnt wait per stage and a workgroup barrier pace the ring.  The
+// stages live in separate LDS arrays: the compiler then knows that a read of
+// one stage cannot alias the copies in flight into the others, and inserts
+// no wait of its own.  Rows are XOR-swizzled in 16-byte chunks so that the
+// MFMA fragment reads of 16 consecutive rows hit distinct banks.
 // ---------------------------------------------------------------------------
 constexpr int kDmaWaves = 8;
 constexpr int kDmaTokens = 32 * kDmaWaves;
-constexpr int kDmaStages = 3;
+#ifndef TREVS_DMA_SLAB
+#define TREVS_DMA_SLAB 128
+#endif
+constexpr int kDmaSlab = TREVS_DMA_SLAB;
+#ifndef TREVS_DMA_RING
+#define TREVS_DMA_RING (kDmaSlab == 128 ? 3 : 6)
+#endif
+constexpr int kDmaRing = TREVS_DMA_RING;
+constexpr int kDmaMaxRing = 6;
+static_assert(kDmaSlab == 64 || kDmaSlab == 128, "slab width");
+static_assert(kDmaRing >= 3 && kDmaRing <= kDmaMaxRing, "ring depth");
 
 // s_waitcnt immediate that waits until at most n vector-memory operations
 // of this wave are outstanding (expcnt and lgkmcnt left unconstrained).
 constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+// Same, and also every LDS access of this wave completed (lgkmcnt 0): placed
+// before a barrier after which another wave's copy may overwrite the buffer.
+constexpr int vmcnt_lds_imm(int n) { return (n & 15) | (7 << 4) | ((n >> 4) << 14); }
 
 __device__ __forceinline__ void lds_dma16(const void* gsrc, uint8_t* lds_wave_base) {
   __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0, 0);
@@ -310,17 +345,30 @@ __device__ __forceinline__ void block_barrier_nofence() {
   asm volatile("" ::: "memory");
 }
 
-template <class In, int MT>
+// Physical 16-byte chunk of logical chunk c in row r of a SLAB-byte row.
+template <int SLAB>
+__device__ __forceinline__ int slab_swizzle(int r, int c) {
+  return SLAB == 128 ? c ^ ((r >> 1) & 7) : c ^ ((r >> 2) & 3);
+}
+
+template <class In, int MT, int SLAB, int RING>
 __global__ __launch_bounds__(64 * kDmaWaves) void relevance_dma_kernel(RelArgs a) {
   constexpr int NT = 64 * kDmaWaves;
   constexpr int VT = kDmaTokens;
   constexpr int MB = MT / 32;
-  constexpr int ZB = VT * 128;
-  constexpr int STAGE = ZB + MT * 128;
-  constexpr int BLK = STAGE / 1024;                    // 1 KB blocks per stage
-  static_assert(BLK % kDmaWaves == 0, "stage blocks must split evenly over the waves");
-  constexpr int BPW = BLK / kDmaWaves;                 // DMA instructions per wave per stage
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kDmaStages * STAGE];
+  constexpr int CPR = SLAB / 16;                // 16-byte chunks per slab row
+  constexpr int RPB = 1024 / SLAB;              // rows per 1 KB copy
+  constexpr int QN = SLAB / 32;                 // 16-byte fragment chunks per lane per slab
+  constexpr int ZBYTES = VT * SLAB;
+  constexpr int STAGE = ZBYTES + MT * SLAB;
+  constexpr int ZPW = ZBYTES / 1024 / kDmaWaves;      // Z copies per wave per stage
+  constexpr int TPW = MT * SLAB / 1024 / kDmaWaves;   // text copies per wave per stage
+  constexpr int OPS = ZPW + TPW;
+  static_assert(ZPW * kDmaWaves * 1024 == ZBYTES && TPW * kDmaWaves * 1024 == MT * SLAB,
+                "a stage must split evenly over the waves");
+  __shared__ __attribute__((aligned(1024))) uint8_t r0[STAGE], r1[STAGE], r2[STAGE],
+      r3[RING > 3 ? STAGE : 16], r4[RING > 4 ? STAGE : 16], r5[RING > 5 ? STAGE : 16];
+  __shared__ float tn[MT];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
@@ -329,97 +377,109 @@ __global__ __launch_bounds__(64 * kDmaWaves) void relevance_dma_kernel(RelArgs a
   const int tok0 = (tile - b * a.tiles_per_sample) * VT;
   const int N = a.N, rb = a.row_bytes;
   const int Mb = a.text_len ? a.text_len[b] : a.M_max;
-  const int n_slabs = rb >> 7;
+  const int n_slabs = rb / SLAB;
+  const int n_iter = (n_slabs + RING - 1) / RING;  // stages padded to the ring depth
+  uint8_t* const ring[kDmaMaxRing] = {r0, r1, r2, r3, r4, r5};
 
-  // ---- saliency of this tile's tokens
-  for (int t = tid; t < VT; t += NT) {
-    const int i = tok0 + t;
-    if (i < N) {
-      const int seg = i / a.seg_len;
-      float acc = 0.f;
-      for (int h = 0; h < a.H; ++h) {
-        const float2 st = a.row_stats[((size_t)b * a.H + h) * a.n_seg + seg];
-        const float x = load_scalar(a.cls, ((size_t)b * a.H + h) * N + i, In{});
-        acc = fmaf(__builtin_amdgcn_exp2f(fmaf(x, kLog2e, -st.x)), st.y, acc);
-      }
-      a.sal[(size_t)b * N + i] = acc / (float)a.H;
-    }
+  const float* itn = a.inv_tnorm + (size_t)b * a.M_max;
+  auto stage_norms = [&](int j0) {  // inverse text norms of a chunk, zero past the text
+    if (tid < MT) tn[tid] = j0 + tid < Mb ? itn[j0 + tid] : 0.f;
+  };
+
+  // sources (slab 0) of this wave's Z copies: row r of the tile, chunk p
+  const int cr = lane / CPR, cp = lane % CPR;
+  const uint8_t* zsrc[ZPW];
+#pragma unroll
+  for (int k = 0; k < ZPW; ++k) {
+    const int r = (wave + kDmaWaves * k) * RPB + cr;
+    zsrc[k] = reinterpret_cast<const uint8_t*>(a.Z) + ((size_t)b * N + min(tok0 + r, N - 1)) * rb +
+              slab_swizzle<SLAB>(r, cp) * 16;
   }
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // only the copies below are counted in the loop
-
-  const uint8_t* zbase = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
   const uint8_t* tbase = reinterpret_cast<const uint8_t*>(a.T) + (size_t)b * a.M_max * rb;
-  const int r8 = lane >> 3, phys = lane & 7;
   const int tok = tok0 + wave * 32 + col;
+  const int zr = wave * 32 + col;  // this lane's Z row in the stage
 
   float zsq = 0.f, rsum = 0.f;
   for (int j0 = 0; j0 < Mb; j0 += MT) {
-    // source row of every 1 KB block this wave copies (slab 0)
-    const uint8_t* src[BPW];
-#pragma unroll
-    for (int k = 0; k < BPW; ++k) {
-      const int blk = wave + kDmaWaves * k;
-      if (blk < VT / 8) {
-        const int row = blk * 8 + r8;
-        src[k] = zbase + (size_t)min(tok0 + row, N - 1) * rb + ((phys ^ (row & 7)) << 4);
-      } else {
-        const int row = (blk - VT / 8) * 8 + r8;
-        src[k] = tbase + (size_t)min(j0 + row, a.M_max - 1) * rb + ((phys ^ (row & 7)) << 4);
-      }
+    if (j0 > 0) {  // the previous chunk's epilogue has read its norms
+      __syncthreads();
+      stage_norms(j0);
     }
-    // stages past the last slab copy row data of slab 0 again (valid, cached)
-    auto issue = [&](int s) {
-      uint8_t* st = lds + (s % kDmaStages) * STAGE;
-      const int off = s < n_slabs ? s * 128 : 0;
+    // the explicit waits below count this wave's memory operations in issue
+    // order, so none may be pending here
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    const uint8_t* tsrc[TPW];
 #pragma unroll
-      for (int k = 0; k < BPW; ++k) lds_dma16(src[k] + off, st + (wave + kDmaWaves * k) * 1024);
+    for (int k = 0; k < TPW; ++k) {
+      const int r = (wave + kDmaWaves * k) * RPB + cr;
+      tsrc[k] = tbase + (size_t)min(j0 + r, a.M_max - 1) * rb + slab_swizzle<SLAB>(r, cp) * 16;
+    }
+    // stage s into ring buffer st; the padding stages past the last slab
+    // re-read the last slab (still in L2) and are never multiplied
+    auto issue = [&](int s, uint8_t* st) {
+      const int off = min(s, n_slabs - 1) * SLAB;
+#pragma unroll
+      for (int k = 0; k < ZPW; ++k) lds_dma16(zsrc[k] + off, st + (wave + kDmaWaves * k) * 1024);
+#pragma unroll
+      for (int k = 0; k < TPW; ++k)
+        lds_dma16(tsrc[k] + off, st + ZBYTES + (wave + kDmaWaves * k) * 1024);
     };
     f32x16 acc[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][r] = 0.f;
-    issue(0);
-    issue(1);
-    for (int s = 0; s < n_slabs; ++s) {
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(BPW));  // this wave's copies of stage s landed
-      block_barrier_nofence();                      // ... and every other wave's
-      issue(s + 2);
-      const uint8_t* st = lds + (s % kDmaStages) * STAGE;
-      u32x4 bf[4];
-      {
-        const int row = wave * 32 + col;
+    auto compute = [&](const uint8_t* st) {
+      u32x4 zf[QN];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          bf[q] = *reinterpret_cast<const u32x4*>(st + row * 128 + (((4 * half + q) ^ (row & 7)) << 4));
-      }
+      for (int q = 0; q < QN; ++q)
+        zf[q] = *reinterpret_cast<const u32x4*>(st + zr * SLAB + slab_swizzle<SLAB>(zr, QN * half + q) * 16);
       if (j0 == 0) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) zsq += sumsq(bf[q], In{});
+        for (int q = 0; q < QN; ++q) zsq += sumsq(zf[q], In{});
       }
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int row = mb * 32 + col;
-        u32x4 af[4];
+        u32x4 af[QN];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          af[q] = *reinterpret_cast<const u32x4*>(st + ZB + row * 128 + (((4 * half + q) ^ (row & 7)) << 4));
-        acc[mb] = mfma_frag(af, bf, acc[mb], In{});
+        for (int q = 0; q < QN; ++q)
+          af[q] = *reinterpret_cast<const u32x4*>(st + ZBYTES + row * SLAB +
+                                                  slab_swizzle<SLAB>(row, QN * half + q) * 16);
+        acc[mb] = mfma_frag(af, zf, acc[mb], In{});
+      }
+    };
+#pragma unroll
+    for (int c = 0; c < RING - 1; ++c) issue(c, ring[c]);
+    if (j0 == 0) {
+      // saliency and the first chunk's norms overlap the first copies; their
+      // loads are younger than the copies, which only makes the waits below
+      // stricter
+      tile_saliency<In>(a, b, tok0, VT, NT, tid);
+      stage_norms(0);
+    }
+    for (int it = 0; it < n_iter; ++it) {
+#pragma unroll
+      for (int c = 0; c < RING; ++c) {
+        const int s = it * RING + c;
+        // stage s landed for this wave (RING - 2 younger stages may be in
+        // flight), then for every wave
+        __builtin_amdgcn_s_waitcnt(vmcnt_lds_imm((RING - 2) * OPS));
+        block_barrier_nofence();
+        issue(s + RING - 1, ring[(c + RING - 1) % RING]);  // the buffer computed last step
+        if (s < n_slabs) compute(ring[c]);
       }
     }
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     block_barrier_nofence();  // the ring is refilled by the next text chunk
     // ---- epilogue of this text chunk: sum_j max(t_j.z_i / ||t_j||, 0)^2
-    const float* itn = a.inv_tnorm + (size_t)b * a.M_max;
+    // (the staged norm is zero for rows past the text, which drops them)
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int j = j0 + mb * 32 + mfma_row(r, half);
-        if (j < Mb) {
-          const float c = fmaxf(acc[mb][r] * itn[j], 0.f);
-          rsum = fmaf(c, c, rsum);
-        }
+        const float c = fmaxf(acc[mb][r] * tn[mb * 32 + mfma_row(r, half)], 0.f);
+        rsum = fmaf(c, c, rsum);
       }
   }
   const float zz = zsq + __shfl_xor(zsq, 32, 64);
@@ -551,7 +611,9 @@ static void launch_rel_t(const RelArgs& a, int MT, hipStream_t s) {
     hipLaunchKernelGGL((relevance_kernel<In, 128, kRelNW, kRelSB>), grid, block, 0, s, a);
 }
 
-bool relevance_uses_dma(int row_bytes, int MT) { return row_bytes % 128 == 0 && MT >= 64; }
+bool relevance_uses_dma(int row_bytes, int MT) {
+  return row_bytes % kDmaSlab == 0 && (MT == 128 || (MT == 64 && kDmaSlab == 128));
+}
 int relevance_tile_tokens_for(int row_bytes, int MT) {
   return relevance_uses_dma(row_bytes, MT) ? kDmaTokens : relevance_tile_tokens();
 }
@@ -560,9 +622,9 @@ template <class In>
 static void launch_rel_dma_t(const RelArgs& a, int MT, hipStream_t s) {
   const dim3 grid(a.B * a.tiles_per_sample), block(64 * kDmaWaves);
   if (MT == 64)
-    hipLaunchKernelGGL((relevance_dma_kernel<In, 64>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((relevance_dma_kernel<In, 64, 128, 3>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((relevance_dma_kernel<In, 128>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((relevance_dma_kernel<In, 128, kDmaSlab, kDmaRing>), grid, block, 0, s, a);
 }
 
 hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s) {
