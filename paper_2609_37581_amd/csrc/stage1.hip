@@ -301,73 +301,48 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Relevance, direct-to-LDS variant (rows made of whole slabs of SLAB bytes,
-// text tile of 64 or 128 rows).  Same arithmetic as relevance_kernel; a
-// workgroup of 8 waves owns 256 tokens.  Each stage (the SLAB-byte slab of
-// the 256 Z rows and of the MT text rows) is copied from memory straight into
-// LDS by global_load_lds (16 bytes per lane, 1 KB per wave instruction,
-// whole slabs of consecutive rows, so every instruction reads full lines)
-// into a ring of RING stages: RING - 1 stages are in flight while one is
-// multiplied.  Every wave issues the same number of copies per stage, so one
-// explicit vmcnt wait per stage and a workgroup barrier pace the ring.  The
-// stages live in separate LDS arrays: the compiler then knows that a read of
-// one stage cannot alias the copies in flight into the others, and inserts
-// no wait of its own.  Rows are XOR-swizzled in 16-byte chunks so that the
-// MFMA fragment reads of 16 consecutive rows hit distinct banks.
+// Relevance, streaming variant for rows made of whole 128-byte slabs and a
+// text tile of 64 or 128 rows.  Same arithmetic as relevance_kernel; a
+// workgroup of 8 waves owns 256 tokens.  Stage s is the 128-byte slab s of
+// the 256 Z rows and of the MT text rows.  Every thread loads its share of a
+// stage with coalesced 16-byte loads (8 lanes cover one 128-byte row
+// segment) into a ring of R register buffers, so R stages are in flight; at
+// each step the oldest buffer is written to one of two LDS buffers, the
+// workgroup synchronises once, and the waves multiply the stage on the
+// matrix cores (plain loads sustain a higher HBM rate on this chip than
+// direct-to-LDS copies).  Rows are XOR-swizzled in 16-byte chunks so that
+// both the stage writes and the MFMA fragment reads of 16 consecutive rows
+// hit distinct banks.  Saliency (Eq. (2)-(3)) is computed while the first
+// stages load.
 // ---------------------------------------------------------------------------
-constexpr int kDmaWaves = 8;
-constexpr int kDmaTokens = 32 * kDmaWaves;
-#ifndef TREVS_DMA_SLAB
-#define TREVS_DMA_SLAB 128
+constexpr int kStreamWaves = 8;
+constexpr int kStreamTokens = 32 * kStreamWaves;
+// register ring depth for text tiles of 128 and 64 rows
+#ifndef TREVS_STREAM_R128
+#define TREVS_STREAM_R128 2
 #endif
-constexpr int kDmaSlab = TREVS_DMA_SLAB;
-#ifndef TREVS_DMA_RING
-#define TREVS_DMA_RING (kDmaSlab == 128 ? 3 : 6)
+#ifndef TREVS_STREAM_R64
+#define TREVS_STREAM_R64 3
 #endif
-constexpr int kDmaRing = TREVS_DMA_RING;
-constexpr int kDmaMaxRing = 6;
-static_assert(kDmaSlab == 64 || kDmaSlab == 128, "slab width");
-static_assert(kDmaRing >= 3 && kDmaRing <= kDmaMaxRing, "ring depth");
+constexpr int kStreamR128 = TREVS_STREAM_R128, kStreamR64 = TREVS_STREAM_R64;
+static_assert(kStreamR128 >= 2 && kStreamR128 <= 4 && kStreamR64 >= 2 && kStreamR64 <= 4,
+              "register ring depth");
 
-// s_waitcnt immediate that waits until at most n vector-memory operations
-// of this wave are outstanding (expcnt and lgkmcnt left unconstrained).
-constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
-// Same, and also every LDS access of this wave completed (lgkmcnt 0): placed
-// before a barrier after which another wave's copy may overwrite the buffer.
-constexpr int vmcnt_lds_imm(int n) { return (n & 15) | (7 << 4) | ((n >> 4) << 14); }
+// Physical 16-byte chunk of logical chunk c in row r of a 128-byte slab row.
+__device__ __forceinline__ int slab_swizzle(int r, int c) { return c ^ ((r >> 1) & 7); }
 
-__device__ __forceinline__ void lds_dma16(const void* gsrc, uint8_t* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0, 0);
-}
-__device__ __forceinline__ void block_barrier_nofence() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-// Physical 16-byte chunk of logical chunk c in row r of a SLAB-byte row.
-template <int SLAB>
-__device__ __forceinline__ int slab_swizzle(int r, int c) {
-  return SLAB == 128 ? c ^ ((r >> 1) & 7) : c ^ ((r >> 2) & 3);
-}
-
-template <class In, int MT, int SLAB, int RING>
-__global__ __launch_bounds__(64 * kDmaWaves) void relevance_dma_kernel(RelArgs a) {
-  constexpr int NT = 64 * kDmaWaves;
-  constexpr int VT = kDmaTokens;
+template <class In, int MT, int R>
+__global__ __launch_bounds__(64 * kStreamWaves) void relevance_stream_kernel(RelArgs a) {
+  constexpr int NT = 64 * kStreamWaves;
+  constexpr int VT = kStreamTokens;
   constexpr int MB = MT / 32;
-  constexpr int CPR = SLAB / 16;                // 16-byte chunks per slab row
-  constexpr int RPB = 1024 / SLAB;              // rows per 1 KB copy
-  constexpr int QN = SLAB / 32;                 // 16-byte fragment chunks per lane per slab
-  constexpr int ZBYTES = VT * SLAB;
-  constexpr int STAGE = ZBYTES + MT * SLAB;
-  constexpr int ZPW = ZBYTES / 1024 / kDmaWaves;      // Z copies per wave per stage
-  constexpr int TPW = MT * SLAB / 1024 / kDmaWaves;   // text copies per wave per stage
-  constexpr int OPS = ZPW + TPW;
-  static_assert(ZPW * kDmaWaves * 1024 == ZBYTES && TPW * kDmaWaves * 1024 == MT * SLAB,
-                "a stage must split evenly over the waves");
-  __shared__ __attribute__((aligned(1024))) uint8_t r0[STAGE], r1[STAGE], r2[STAGE],
-      r3[RING > 3 ? STAGE : 16], r4[RING > 4 ? STAGE : 16], r5[RING > 5 ? STAGE : 16];
+  constexpr int ZBYTES = VT * 128;
+  constexpr int STAGE = ZBYTES + MT * 128;
+  constexpr int ZPT = ZBYTES / 16 / NT;        // Z chunks per thread per stage
+  constexpr int TPT = MT * 128 / 16 / NT;      // text chunks per thread per stage
+  constexpr int U = R % 2 ? 2 * R : R;         // steps per unrolled iteration
+  static_assert(ZPT * NT * 16 == ZBYTES && TPT * NT * 16 == MT * 128, "stage split");
+  __shared__ __attribute__((aligned(1024))) uint8_t l0[STAGE], l1[STAGE];
   __shared__ float tn[MT];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -377,52 +352,57 @@ __global__ __launch_bounds__(64 * kDmaWaves) void relevance_dma_kernel(RelArgs a
   const int tok0 = (tile - b * a.tiles_per_sample) * VT;
   const int N = a.N, rb = a.row_bytes;
   const int Mb = a.text_len ? a.text_len[b] : a.M_max;
-  const int n_slabs = rb / SLAB;
-  const int n_iter = (n_slabs + RING - 1) / RING;  // stages padded to the ring depth
-  uint8_t* const ring[kDmaMaxRing] = {r0, r1, r2, r3, r4, r5};
+  const int n_slabs = rb >> 7;
+  const int n_iter = (n_slabs + U - 1) / U;  // stages padded to the unroll
 
   const float* itn = a.inv_tnorm + (size_t)b * a.M_max;
   auto stage_norms = [&](int j0) {  // inverse text norms of a chunk, zero past the text
     if (tid < MT) tn[tid] = j0 + tid < Mb ? itn[j0 + tid] : 0.f;
   };
 
-  // sources (slab 0) of this wave's Z copies: row r of the tile, chunk p
-  const int cr = lane / CPR, cp = lane % CPR;
-  const uint8_t* zsrc[ZPW];
+  // chunk k of this thread in a stage: row (tid / 8 + 64 k), chunk (tid % 8)
+  const int cr = tid >> 3, cc = tid & 7;
+  // (rows 64 apart share the swizzle, so the LDS offsets differ by 8 KB)
+  const uint8_t* zsrc[ZPT];
 #pragma unroll
-  for (int k = 0; k < ZPW; ++k) {
-    const int r = (wave + kDmaWaves * k) * RPB + cr;
-    zsrc[k] = reinterpret_cast<const uint8_t*>(a.Z) + ((size_t)b * N + min(tok0 + r, N - 1)) * rb +
-              slab_swizzle<SLAB>(r, cp) * 16;
+  for (int k = 0; k < ZPT; ++k) {
+    const int r = cr + (NT / 8) * k;
+    zsrc[k] = reinterpret_cast<const uint8_t*>(a.Z) + ((size_t)b * N + min(tok0 + r, N - 1)) * rb + cc * 16;
   }
+  const int sdst = cr * 128 + slab_swizzle(cr, cc) * 16;
   const uint8_t* tbase = reinterpret_cast<const uint8_t*>(a.T) + (size_t)b * a.M_max * rb;
   const int tok = tok0 + wave * 32 + col;
   const int zr = wave * 32 + col;  // this lane's Z row in the stage
 
   float zsq = 0.f, rsum = 0.f;
   for (int j0 = 0; j0 < Mb; j0 += MT) {
-    if (j0 > 0) {  // the previous chunk's epilogue has read its norms
+    const bool first = j0 == 0;
+    if (!first) {  // the previous chunk's epilogue has read its norms
       __syncthreads();
       stage_norms(j0);
     }
-    // the explicit waits below count this wave's memory operations in issue
-    // order, so none may be pending here
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    const uint8_t* tsrc[TPW];
+    const uint8_t* tsrc[TPT];
 #pragma unroll
-    for (int k = 0; k < TPW; ++k) {
-      const int r = (wave + kDmaWaves * k) * RPB + cr;
-      tsrc[k] = tbase + (size_t)min(j0 + r, a.M_max - 1) * rb + slab_swizzle<SLAB>(r, cp) * 16;
+    for (int k = 0; k < TPT; ++k) {
+      const int r = cr + (NT / 8) * k;
+      tsrc[k] = tbase + (size_t)min(j0 + r, a.M_max - 1) * rb + cc * 16;
     }
-    // stage s into ring buffer st; the padding stages past the last slab
+    // stage s into register buffer g; the padding stages past the last slab
     // re-read the last slab (still in L2) and are never multiplied
-    auto issue = [&](int s, uint8_t* st) {
-      const int off = min(s, n_slabs - 1) * SLAB;
+    u32x4 g[R][ZPT + TPT];
+    auto load = [&](int s, u32x4 (&dst)[ZPT + TPT]) {
+      const int off = min(s, n_slabs - 1) * 128;
 #pragma unroll
-      for (int k = 0; k < ZPW; ++k) lds_dma16(zsrc[k] + off, st + (wave + kDmaWaves * k) * 1024);
+      for (int k = 0; k < ZPT; ++k) dst[k] = ldg16_stream(zsrc[k] + off);
 #pragma unroll
-      for (int k = 0; k < TPW; ++k)
-        lds_dma16(tsrc[k] + off, st + ZBYTES + (wave + kDmaWaves * k) * 1024);
+      for (int k = 0; k < TPT; ++k) dst[ZPT + k] = ldg16(tsrc[k] + off);
+    };
+    auto store = [&](uint8_t* st, const u32x4 (&src)[ZPT + TPT]) {
+#pragma unroll
+      for (int k = 0; k < ZPT; ++k) *reinterpret_cast<u32x4*>(st + sdst + k * (NT / 8) * 128) = src[k];
+#pragma unroll
+      for (int k = 0; k < TPT; ++k)
+        *reinterpret_cast<u32x4*>(st + ZBYTES + sdst + k * (NT / 8) * 128) = src[ZPT + k];
     };
     f32x16 acc[MB];
 #pragma unroll
@@ -430,48 +410,44 @@ __global__ __launch_bounds__(64 * kDmaWaves) void relevance_dma_kernel(RelArgs a
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][r] = 0.f;
     auto compute = [&](const uint8_t* st) {
-      u32x4 zf[QN];
+      u32x4 zf[4];
 #pragma unroll
-      for (int q = 0; q < QN; ++q)
-        zf[q] = *reinterpret_cast<const u32x4*>(st + zr * SLAB + slab_swizzle<SLAB>(zr, QN * half + q) * 16);
+      for (int q = 0; q < 4; ++q)
+        zf[q] = *reinterpret_cast<const u32x4*>(st + zr * 128 + slab_swizzle(zr, 4 * half + q) * 16);
       if (j0 == 0) {
 #pragma unroll
-        for (int q = 0; q < QN; ++q) zsq += sumsq(zf[q], In{});
+        for (int q = 0; q < 4; ++q) zsq += sumsq(zf[q], In{});
       }
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int row = mb * 32 + col;
-        u32x4 af[QN];
+        u32x4 af[4];
 #pragma unroll
-        for (int q = 0; q < QN; ++q)
-          af[q] = *reinterpret_cast<const u32x4*>(st + ZBYTES + row * SLAB +
-                                                  slab_swizzle<SLAB>(row, QN * half + q) * 16);
+        for (int q = 0; q < 4; ++q)
+          af[q] = *reinterpret_cast<const u32x4*>(st + ZBYTES + row * 128 + slab_swizzle(row, 4 * half + q) * 16);
         acc[mb] = mfma_frag(af, zf, acc[mb], In{});
       }
     };
 #pragma unroll
-    for (int c = 0; c < RING - 1; ++c) issue(c, ring[c]);
-    if (j0 == 0) {
-      // saliency and the first chunk's norms overlap the first copies; their
-      // loads are younger than the copies, which only makes the waits below
-      // stricter
+    for (int c = 0; c < R; ++c) load(c, g[c]);
+    if (first) {
       tile_saliency<In>(a, b, tok0, VT, NT, tid);
       stage_norms(0);
     }
     for (int it = 0; it < n_iter; ++it) {
 #pragma unroll
-      for (int c = 0; c < RING; ++c) {
-        const int s = it * RING + c;
-        // stage s landed for this wave (RING - 2 younger stages may be in
-        // flight), then for every wave
-        __builtin_amdgcn_s_waitcnt(vmcnt_lds_imm((RING - 2) * OPS));
-        block_barrier_nofence();
-        issue(s + RING - 1, ring[(c + RING - 1) % RING]);  // the buffer computed last step
-        if (s < n_slabs) compute(ring[c]);
+      for (int c = 0; c < U; ++c) {
+        const int s = it * U + c;
+        uint8_t* st = c % 2 ? l1 : l0;
+        // buffer (s % 2) was last read at step s - 2, before every wave
+        // passed the barrier of step s - 1
+        store(st, g[c % R]);
+        load(s + R, g[c % R]);
+        __syncthreads();
+        if (s < n_slabs) compute(st);
       }
     }
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    block_barrier_nofence();  // the ring is refilled by the next text chunk
+    __syncthreads();  // the LDS buffers are refilled by the next text chunk
     // ---- epilogue of this text chunk: sum_j max(t_j.z_i / ||t_j||, 0)^2
     // (the staged norm is zero for rows past the text, which drops them)
 #pragma unroll
@@ -611,28 +587,26 @@ static void launch_rel_t(const RelArgs& a, int MT, hipStream_t s) {
     hipLaunchKernelGGL((relevance_kernel<In, 128, kRelNW, kRelSB>), grid, block, 0, s, a);
 }
 
-bool relevance_uses_dma(int row_bytes, int MT) {
-  return row_bytes % kDmaSlab == 0 && (MT == 128 || (MT == 64 && kDmaSlab == 128));
-}
+bool relevance_uses_stream(int row_bytes, int MT) { return row_bytes % 128 == 0 && MT >= 64; }
 int relevance_tile_tokens_for(int row_bytes, int MT) {
-  return relevance_uses_dma(row_bytes, MT) ? kDmaTokens : relevance_tile_tokens();
+  return relevance_uses_stream(row_bytes, MT) ? kStreamTokens : relevance_tile_tokens();
 }
 
 template <class In>
-static void launch_rel_dma_t(const RelArgs& a, int MT, hipStream_t s) {
-  const dim3 grid(a.B * a.tiles_per_sample), block(64 * kDmaWaves);
+static void launch_rel_stream_t(const RelArgs& a, int MT, hipStream_t s) {
+  const dim3 grid(a.B * a.tiles_per_sample), block(64 * kStreamWaves);
   if (MT == 64)
-    hipLaunchKernelGGL((relevance_dma_kernel<In, 64, 128, 3>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((relevance_stream_kernel<In, 64, kStreamR64>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((relevance_dma_kernel<In, 128, kDmaSlab, kDmaRing>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((relevance_stream_kernel<In, 128, kStreamR128>), grid, block, 0, s, a);
 }
 
 hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s) {
-  if (relevance_uses_dma(a.row_bytes, MT)) {
+  if (relevance_uses_stream(a.row_bytes, MT)) {
     if (dtype == 1)
-      launch_rel_dma_t<BF16>(a, MT, s);
+      launch_rel_stream_t<BF16>(a, MT, s);
     else
-      launch_rel_dma_t<F32>(a, MT, s);
+      launch_rel_stream_t<F32>(a, MT, s);
   } else if (dtype == 1) {
     launch_rel_t<BF16>(a, MT, s);
   } else {
