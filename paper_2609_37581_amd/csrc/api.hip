@@ -204,14 +204,6 @@ trevs_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   return TREVS_OK;
 }
 
-int tpr_log2_for(int row_bytes) {
-  const int vpr = row_bytes / 16;
-  const int want = (vpr + 3) / 4;
-  int l = 0;
-  while ((1 << l) < want && l < 8) ++l;
-  return l;
-}
-
 }  // namespace
 
 #define TREVS_TRY(x)                            \
@@ -352,7 +344,6 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   ga.t[0].row_bytes = a->d * e;
   ga.t[0].src_bstride = (long long)a->N * a->d * e;
   ga.t[0].dst_bstride = (long long)a->k_keep * a->d * e;
-  ga.t[0].tpr_log2 = tpr_log2_for(a->d * e);
   ga.n_tensors = 1;
   ga.idx = a->kept_idx;
   ga.B = a->B;
@@ -457,7 +448,6 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
     ga.t[t].row_bytes = rowb[t];
     ga.t[t].src_bstride = (long long)a->S * rowb[t];
     ga.t[t].dst_bstride = (long long)So * rowb[t];
-    ga.t[t].tpr_log2 = tpr_log2_for(rowb[t]);
   }
   ga.n_tensors = 3;
   ga.idx = a->kept_idx;

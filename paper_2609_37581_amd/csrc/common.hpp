@@ -95,6 +95,24 @@ __device__ __forceinline__ void stg16_stream(void* p, u32x4 v) {
 
 __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 
+// Word 3 of a raw (unstructured, stride 0) buffer resource on gfx9-family
+// GPUs: 32-bit data format, bounds checked against num_records.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+// Cache-policy operand of buffer/global memory builtins: nontemporal (data
+// streamed once, not worth keeping in the caches).
+constexpr int kCachePolicyStream = 2;
+
+// Wait until at most n vector-memory operations of this wave are outstanding
+// (s_waitcnt immediate with expcnt and lgkmcnt unconstrained).  Placed where
+// every path reaches it, it also tells the compiler that older loads have
+// landed, so loads issued under uniform branches are not waited for one by
+// one afterwards.
+template <int n>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
+}
+
 // ---------------------------------------------------------------- reductions
 // Wave-wide reductions and scans on DPP lane moves (no LDS traffic): four
 // row_shr steps combine the 16 lanes of a row, then row_bcast:15 and

@@ -20,35 +20,38 @@ __device__ __forceinline__ int src_row(const GatherArgs& a, int b, int r) {
   return r - a.n_kept + a.K_in;
 }
 
+// Buffer resource over one row: accesses at or past `bytes` read zero and
+// write nothing, which masks the tail of a row without any branch.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, bytes, kBufferRsrcWord3);
+}
+
+// Each wave copies one output row, kGatherBatch 1 KB segments at a time: all
+// loads of a batch are issued before the first store, and the row's buffer
+// bounds drop the segments past its end (rows up to 8 KB take one batch; the
+// small batch keeps occupancy high).
 __global__ __launch_bounds__(kGatherThreads) void gather_kernel(GatherArgs a) {
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b = blockIdx.y, z = blockIdx.z;
   const int r0 = blockIdx.x * kGatherRowsPerBlock;
   if (z < a.n_tensors) {
+    static_assert(kGatherRowsPerBlock == kGatherThreads / 64, "one row per wave");
+    const int row = r0 + wave;
+    if (row >= a.rows_out) return;
     const GatherTensor t = a.t[z];
-    const int tpr = 1 << t.tpr_log2;
-    const int sub = tid >> t.tpr_log2, v0 = tid & (tpr - 1);
-    const int vpr = t.row_bytes >> 4;
-    const int rows_par = kGatherThreads >> t.tpr_log2;
-    for (int rr = sub; rr < kGatherRowsPerBlock; rr += rows_par) {
-      const int ro = r0 + rr;
-      if (ro >= a.rows_out) break;
-      const int ri = src_row(a, b, ro);
-      const uint8_t* src = t.src + (size_t)b * t.src_bstride + (size_t)ri * t.row_bytes;
-      uint8_t* dst = t.dst + (size_t)b * t.dst_bstride + (size_t)ro * t.row_bytes;
-      for (int v = v0; v < vpr; v += 4 * tpr) {
-        u32x4 x[4];
+    const __amdgpu_buffer_rsrc_t src =
+        row_rsrc(t.src + (size_t)b * t.src_bstride + (size_t)src_row(a, b, row) * t.row_bytes, t.row_bytes);
+    const __amdgpu_buffer_rsrc_t dst =
+        row_rsrc(t.dst + (size_t)b * t.dst_bstride + (size_t)row * t.row_bytes, t.row_bytes);
+    // (the whole offset goes in the bounds-checked vector operand)
+    for (int o = lane * 16; o < t.row_bytes; o += kGatherBatch * 1024) {
+      u32x4 x[kGatherBatch];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int vv = v + u * tpr;
-          x[u] = vv < vpr ? ldg16(src + (size_t)vv * 16) : zero4();
-        }
+      for (int k = 0; k < kGatherBatch; ++k)
+        x[k] = __builtin_amdgcn_raw_buffer_load_b128(src, o + k * 1024, 0, kCachePolicyStream);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int vv = v + u * tpr;
-          if (vv < vpr) stg16_stream(dst + (size_t)vv * 16, x[u]);
-        }
-      }
+      for (int k = 0; k < kGatherBatch; ++k) __builtin_amdgcn_raw_buffer_store_b128(x[k], dst, o + k * 1024, 0, 0);
     }
     return;
   }

@@ -90,7 +90,6 @@ struct GatherTensor {
   uint8_t* dst;
   long long src_bstride, dst_bstride;  // bytes per sample
   int row_bytes;                       // multiple of 16
-  int tpr_log2;                        // log2(threads per row), threads per row <= 256
 };
 struct GatherArgs {
   GatherTensor t[kGatherMaxTensors];
@@ -101,8 +100,9 @@ struct GatherArgs {
   int64_t* pos_out;          // [n_pos,B,rows_out]
   int n_pos, S;
 };
-constexpr int kGatherRowsPerBlock = 16;
+constexpr int kGatherRowsPerBlock = 4;  // one row per wave
 constexpr int kGatherThreads = 256;
+constexpr int kGatherBatch = 8;  // 16-byte loads in flight per lane
 
 hipError_t launch_prep(const PrepArgs& a, int dtype, hipStream_t s);
 hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s);
