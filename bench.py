@@ -9,6 +9,7 @@ launch stream), and the CPU oracle's rate on a bounded sample of the same
 workload."""
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -36,6 +37,28 @@ def algorithmic_bytes(w, text_len):
     stage2 = (B * e * (m_bar * w.H_q * w.d_h + w.K1 * w.H_kv * w.d_h)
               + B * (2 * So * w.D * e + 4 * So * w.H_kv * w.d_h * e + 2 * w.n_pos * So * 8 + 4 * w.K2))
     return dict(relevance=rel, stage1=stage1, stage2=stage2, total=stage1 + stage2)
+
+
+def counter_traffic(workload):
+    """HBM bytes per relevance launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, each scaled by what the counter reads
+    for a plain copy of known size), or None when that summary is missing or
+    was taken from other kernel sources than the ones built now."""
+    path = os.path.join(ROOT, "profiles", f"hbm_counters_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path).read().splitlines():
+        k, sep, v = line.partition(": ")
+        if sep and k in ("source_sha256", "hbm_bytes_per_launch"):
+            vals[k] = v.strip()
+    h = hashlib.sha256()
+    for f in ("stage1.hip", "common.hpp", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2609_37581_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if vals.get("source_sha256") != h.hexdigest() or "hbm_bytes_per_launch" not in vals:
+        return None
+    return float(vals["hbm_bytes_per_launch"])
 
 
 def cpu_baseline(w, s1, s2, budget_s):
@@ -167,6 +190,7 @@ def main():
     del src, dst
 
     nb = algorithmic_bytes(w, s1["text_len"])
+    traffic = counter_traffic(w.name)
     rel_s = rel_ms * 1e-3
     achieved = nb["relevance"] / rel_s / 1e9
     t_step = ms_step * 1e-3
@@ -189,7 +213,7 @@ def main():
                    "D": w.D, "n_keep_heads": w.n_keep, "P": w.P, "S": w.S},
         "roofline": {"bound": "hbm", "kernel": "prellm.relevance", "achieved": achieved,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": None, "bytes_per_launch": nb["relevance"]},
+                     "traffic": traffic, "bytes_per_launch": nb["relevance"]},
         "path_hbm_frac": nb["total"] / t_step / 1e9 / HBM_PEAK_GBPS,
         "path_bytes": nb,
         "relevance_us": rel_ms * 1e3,
