@@ -1,11 +1,17 @@
 // Stage 2 (in-LLM) kernels: text->vision attention statistics, head variance
 // and high-variance head set, and the token score (Sec. 4.2, Eq. (8)-(9)).
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace trevs {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Key tiles in flight per statistics workgroup: 8 vectors of 16 bytes per
+// thread in registers (even, at least 2).
+constexpr int stats_ring(int vectors_per_tile) { return vectors_per_tile >= 4 ? 2 : 8 / vectors_per_tile; }
 
 // ---------------------------------------------------------------------------
 // Statistics pass.  For every (query head h, text row q) the row of logits
@@ -78,8 +84,13 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
     }
   };
 
+  // Online (max, sum e, sum e^2) in log2 units.  The logit scale is positive,
+  // so the tile maximum is taken on the raw dot products and scaled once, and
+  // each term is exp2(fma(dot, scale, -max)): about four vector operations
+  // and one exp per logit.  Only a split's last tile can hold keys past its
+  // end; it alone takes the masked path.
   float m = -INFINITY, l = 0.f, l2 = 0.f;
-  auto process = [&](int buf, int ib) {
+  auto process = [&](int buf, int ib, auto full) {
     f32x16 acc;
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
@@ -91,20 +102,21 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
       for (int j = 0; j < 4; ++j) kf[j] = *reinterpret_cast<const u32x4*>(p + f * 64 + j * 16);
       acc = mfma_frag(kf, qf[f], acc, In{});
     }
-    float y[16];
-    float mb = -INFINITY;
+    if constexpr (!decltype(full)::value) {
 #pragma unroll
-    for (int rr = 0; rr < 16; ++rr) {
-      y[rr] = (ib + mfma_row(rr, half) < i_end) ? acc[rr] * a.scale_log2e : -INFINITY;
-      mb = fmaxf(mb, y[rr]);
+      for (int rr = 0; rr < 16; ++rr)
+        if (ib + mfma_row(rr, half) >= i_end) acc[rr] = -INFINITY;
     }
-    if (mb > -INFINITY) {
-      const float mn = fmaxf(m, mb);
+    float mx = acc[0];
+#pragma unroll
+    for (int rr = 1; rr < 16; ++rr) mx = fmaxf(mx, acc[rr]);
+    const float mn = fmaxf(m, mx * a.scale_log2e);
+    if (decltype(full)::value || mn > -INFINITY) {
       const float c = fast_exp2(m - mn);
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
-        const float e = fast_exp2(y[rr] - mn);
+        const float e = fast_exp2(fmaf(acc[rr], a.scale_log2e, -mn));
         s1 += e;
         s2 = fmaf(e, e, s2);
       }
@@ -113,21 +125,30 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
       m = mn;
     }
   };
-  // two LDS tiles alternate: one is reduced while the other is filled
-  u32x4 tA[TVT], tB[TVT];
-  load_tile(i_begin, tA);
-  load_tile(i_begin + 32, tB);
-  store_tile(0, tA);
-  __syncthreads();
-  for (int ib = i_begin; ib < i_end; ib += 64) {
-    process(0, ib);
-    store_tile(1, tB);
-    load_tile(ib + 64, tA);
-    __syncthreads();
-    process(1, ib + 32);
-    store_tile(0, tA);
-    load_tile(ib + 96, tB);
-    __syncthreads();
+  // key tiles stream through a ring of RING register buffers (that many
+  // tiles in flight from memory) into two alternating LDS buffers; the tiles
+  // past the split are loaded (row i_begin again) but never reduced
+  constexpr int RING = stats_ring(TVT);
+  const int n_tiles = (i_end - i_begin + 31) / 32;
+  const int n_iter = (n_tiles + RING - 1) / RING;
+  u32x4 ring[RING][TVT];
+#pragma unroll
+  for (int c = 0; c < RING; ++c) load_tile(i_begin + 32 * c, ring[c]);
+  for (int it = 0; it < n_iter; ++it) {
+#pragma unroll
+    for (int c = 0; c < RING; ++c) {
+      const int t = it * RING + c;
+      // LDS buffer (t % 2) was last read at tile t - 2, before every wave
+      // passed the barrier of tile t - 1
+      store_tile(c % 2, ring[c]);
+      load_tile(i_begin + 32 * (t + RING), ring[c]);
+      __syncthreads();
+      const int ib = i_begin + 32 * t;
+      if (ib + 32 <= i_end)
+        process(c % 2, ib, std::true_type{});
+      else if (t < n_tiles)
+        process(c % 2, ib, std::false_type{});
+    }
   }
   const float mo = __shfl_xor(m, 32, 64), lo = __shfl_xor(l, 32, 64), l2o = __shfl_xor(l2, 32, 64);
   const float M = fmaxf(m, mo);
