@@ -76,7 +76,18 @@ typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
  *            rho = 0.5 is Eq. (7) exactly, rho = 0 is [CLS]-only saliency).
  *   kept_idx[b]   = TopK(s, k_keep) in ascending order
  *   kept_feats[b] = vis_feats[b, kept_idx[b], :]  (bit copy)
+ * With ratio_mode = TREVS_RATIO_BUDGET the textual ratio is instead the
+ * share of the token budget given to textual relevance (the reading of the
+ * preliminary analysis, Sec. 3): K_t = floor(rho * k_keep + 1/2) tokens with
+ * the highest s^t, then the k_keep - K_t tokens with the highest s^v among
+ * the others; Eq. (6)-(7) are not used, and score_out and norm_stats must
+ * be NULL.  Every top-K is stable (score descending, lower index first).
  * ---------------------------------------------------------------------- */
+typedef enum trevs_ratio_mode {
+  TREVS_RATIO_WEIGHTS = 0, /* branch weights 2(1-rho), 2rho inside Eq. (7) */
+  TREVS_RATIO_BUDGET = 1   /* budget split between s^t and s^v */
+} trevs_ratio_mode;
+
 typedef struct trevs_prellm_args {
   uint32_t struct_size;      /* sizeof(trevs_prellm_args) */
   int32_t B;                 /* samples */
@@ -103,6 +114,7 @@ typedef struct trevs_prellm_args {
   float* rel_out;            /* OPTIONAL OUT [B,N] s^t */
   float* norm_stats;         /* OPTIONAL OUT [B,4] Med(s^v), MAD(s^v), Med(s^t), MAD(s^t) */
   void* const* events;       /* OPTIONAL [2*TREVS_PRELLM_NUM_KERNELS] hipEvent_t */
+  int32_t ratio_mode;        /* trevs_ratio_mode */
 } trevs_prellm_args;
 
 /* ------------------------------------------------------------------------

@@ -148,6 +148,24 @@ def topk_ascending(scores, k):
     return np.array(sorted(order[:k]), dtype=np.int64)
 
 
+def budget_split_topk(sv, st, k, rho):
+    """The "textual ratio" read as in the preliminary analysis (Sec. 3): the
+    share of a token budget filled by textual relevance.  K_t = floor(rho k +
+    1/2) tokens with the highest s^t, then the k - K_t tokens with the highest
+    s^v among the others (each ranking: score descending, index ascending).
+    Returns the union as ascending indices."""
+    sv = np.asarray(sv, dtype=np.float64)
+    st = np.asarray(st, dtype=np.float64)
+    n = sv.size
+    if not 0 <= k <= n:
+        raise ValueError("k out of range")
+    k_t = min(max(int(math.floor(rho * k + 0.5)), 0), k)
+    by_text = [i for i in sorted(range(n), key=lambda i: (-st[i], i))][:k_t]
+    taken = set(by_text)
+    rest = [i for i in sorted(range(n), key=lambda i: (-sv[i], i)) if i not in taken]
+    return np.array(sorted(by_text + rest[:k - k_t]), dtype=np.int64)
+
+
 def farthest_point_sampling(Z, selected, k_div):
     """Context preservation (Sec. 4.1, after Eq. (7)): k_div tokens taken one at
     a time from the candidates outside `selected`, each the candidate whose
@@ -175,19 +193,26 @@ def farthest_point_sampling(Z, selected, k_div):
 
 
 def prellm_sample(cls_logits, Z, T, *, n_seg=1, k_keep, k_div=0, rho=0.5,
-                  tau_v=1.4, tau_t=1.0, lam=1.0, eps=1e-8):
+                  tau_v=1.4, tau_t=1.0, lam=1.0, eps=1e-8, ratio_mode="weights"):
     """Stage 1 for one sample (Sec. 4.1), all inputs float64.
 
     cls_logits [H_v, N]; Z [N, d']; T [M_b, d'] (valid text rows only).
     Returns a dict with s^v, s^t, the normalised scores, the fused score s,
-    the medians / MADs, and kept_idx (ascending, K_1 = k_keep entries)."""
+    the medians / MADs, and kept_idx (ascending, K_1 = k_keep entries).
+    ratio_mode "budget" takes the pivots by budget_split_topk on the raw
+    scores instead of Eq. (6)-(7)."""
     sv = cls_saliency(cls_logits, n_seg)
     st = text_relevance(Z, T)
     sv_hat, med_v, mad_v = robust_normalise(sv, tau_v, eps)
     st_hat, med_t, mad_t = robust_normalise(st, tau_t, eps)
     s = fuse_scores(sv_hat, st_hat, rho, lam)
     k_piv = k_keep - k_div
-    pivots = topk_ascending(s, k_piv)
+    if ratio_mode == "budget":
+        pivots = budget_split_topk(sv, st, k_piv, rho)
+    elif ratio_mode == "weights":
+        pivots = topk_ascending(s, k_piv)
+    else:
+        raise ValueError("ratio_mode")
     extra = farthest_point_sampling(Z, pivots, k_div) if k_div else np.zeros(0, np.int64)
     kept = np.sort(np.concatenate([pivots, extra]))
     return dict(sal=sv, rel=st, sal_hat=sv_hat, rel_hat=st_hat, score=s,
@@ -196,7 +221,7 @@ def prellm_sample(cls_logits, Z, T, *, n_seg=1, k_keep, k_div=0, rho=0.5,
 
 
 def prellm(cls_logits, Z, T, text_len, dtype, *, n_seg=1, k_keep, k_div=0,
-           rho=0.5, tau_v=1.4, tau_t=1.0, lam=1.0, eps=1e-8):
+           rho=0.5, tau_v=1.4, tau_t=1.0, lam=1.0, eps=1e-8, ratio_mode="weights"):
     """Stage 1 over a batch.  Array inputs are in the library's storage form
     (float32, or uint16 bf16 bits): cls_logits [B,H_v,N], Z [B,N,d'],
     T [B,M_max,d'], text_len [B] or None.  kept_feats is the row gather of the
@@ -212,7 +237,7 @@ def prellm(cls_logits, Z, T, text_len, dtype, *, n_seg=1, k_keep, k_div=0,
         r = prellm_sample(to_f64(cls_logits[b], dtype), to_f64(Z[b], dtype),
                           to_f64(T[b, :mb], dtype), n_seg=n_seg, k_keep=k_keep,
                           k_div=k_div, rho=rho, tau_v=tau_v, tau_t=tau_t,
-                          lam=lam, eps=eps)
+                          lam=lam, eps=eps, ratio_mode=ratio_mode)
         for key in ("sal", "rel", "score", "kept_idx", "med_v", "mad_v",
                     "med_t", "mad_t"):
             out[key].append(r[key])

@@ -1,6 +1,7 @@
 // Host side of the C ABI: argument validation, workspace layout and the
 // launch sequence of each stage.  Nothing here allocates device memory or
 // waits for the device.
+#include <cmath>
 #include <math.h>
 #include <string.h>
 
@@ -92,9 +93,17 @@ trevs_status validate_prellm(const trevs_prellm_args* a) {
                       {a->rel_out, a->rel_out ? B * N * 4 : 0},
                       {a->norm_stats, a->norm_stats ? B * 16 : 0}};
   if (any_overlap(out, 6, in, 4)) return TREVS_ERR_INVALID_ARG;
+  if (a->ratio_mode != TREVS_RATIO_WEIGHTS && a->ratio_mode != TREVS_RATIO_BUDGET) return TREVS_ERR_INVALID_ARG;
+  if (a->ratio_mode == TREVS_RATIO_BUDGET && (a->score_out || a->norm_stats)) return TREVS_ERR_INVALID_ARG;
   if (a->k_div > 0) return TREVS_ERR_UNSUPPORTED;
   if (a->N > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
   return TREVS_OK;
+}
+
+// Tokens chosen by textual relevance in the budget-split mode: floor(rho K + 1/2).
+int budget_text_count(float rho, int K) {
+  const int kt = (int)std::floor((double)rho * K + 0.5);
+  return std::min(std::max(kt, 0), K);
 }
 
 PrellmLayout prellm_layout(const trevs_prellm_args* a) {
@@ -308,6 +317,7 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   TREVS_HIP(launch_relevance(ra, a->dtype, MT, s));
   TREVS_TRY(record(a->events, 3, s));
 
+  const bool budget = a->ratio_mode == TREVS_RATIO_BUDGET;
   float* stats = reinterpret_cast<float*>(w + L.stats);
   NormArgs na;
   na.sal = sal;
@@ -315,7 +325,7 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   na.N = a->N;
   na.stats = stats;
   TREVS_TRY(record(a->events, 4, s));
-  TREVS_HIP(launch_norm_stats(na, a->B, s));
+  if (!budget) TREVS_HIP(launch_norm_stats(na, a->B, s));  // the budget split ranks raw scores
   TREVS_TRY(record(a->events, 5, s));
 
   SelArgs sa;
@@ -333,8 +343,12 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   sa.score_out = a->score_out;
   sa.norm_stats = a->norm_stats;
   sa.kept_idx = a->kept_idx;
+  sa.K_t = budget_text_count(a->textual_ratio, a->k_keep);
   TREVS_TRY(record(a->events, 6, s));
-  TREVS_HIP(launch_prellm_select(sa, a->B, s));
+  if (budget)
+    TREVS_HIP(launch_budget_select(sa, a->B, s));
+  else
+    TREVS_HIP(launch_prellm_select(sa, a->B, s));
   TREVS_TRY(record(a->events, 7, s));
 
   GatherArgs ga;

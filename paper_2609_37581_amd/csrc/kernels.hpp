@@ -44,6 +44,7 @@ struct SelArgs {
   const float* rel;
   const float* stats;        // [B,4] from the robust-statistics kernel
   int N, K;
+  int K_t;                   // budget-split mode: tokens taken by s^t first
   float wv, wt, tau_v, tau_t, lam, eps;
   float* score_out;          // [B,N] or null
   float* norm_stats;         // [B,4] or null
@@ -111,6 +112,9 @@ int relevance_tile_tokens();
 int relevance_tile_tokens_for(int row_bytes, int MT);
 hipError_t launch_norm_stats(const NormArgs& a, int B, hipStream_t s);
 hipError_t launch_prellm_select(const SelArgs& a, int B, hipStream_t s);
+// Budget-split selection: the K_t highest s^t, then the K - K_t highest s^v
+// among the other tokens.
+hipError_t launch_budget_select(const SelArgs& a, int B, hipStream_t s);
 hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, hipStream_t s);
 hipError_t launch_stats(const StatsArgs& a, int dtype, int dh, hipStream_t s);
 hipError_t launch_heads(const HeadArgs& a, hipStream_t s);

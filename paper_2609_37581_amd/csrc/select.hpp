@@ -266,15 +266,20 @@ __device__ __forceinline__ void wcnt_scan(int n, SelectShared& sh) {
   __syncthreads();
 }
 
-// Stable top-K: keep every element whose score is above the K-th largest and
-// the lowest-index elements equal to it, and write the kept indices in
-// ascending order to out[0..K).
-template <int E>
-__device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* out,
-                                 SelectShared& sh) {
+// Stable top-K as a mask: bit e of the result is set when this thread's
+// element e is kept, i.e. its key is above the K-th largest, or equal to it
+// and among the lowest-index elements of that key (K in 0..N).
+template <int E, class KeyF>
+__device__ uint32_t block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  auto keyf = [&](int e) { return f2key(sc[e]); };
   auto valid = [&](int e) { return e * kSelThreads + tid < N; };
+  if (K <= 0) return 0u;
+  if (K >= N) {
+    uint32_t all = 0u;
+#pragma unroll
+    for (int e = 0; e < E; ++e) all |= valid(e) ? (1u << e) : 0u;
+    return all;
+  }
   uint32_t thr;
   int less, eq;
   block_select<E>(keyf, N, N - K, thr, less, eq, sh);
@@ -300,19 +305,41 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
     const bool keep = valid(e) && (keyf(e) > thr || (eqe && eq_rank < need_eq));
     keep_mask |= keep ? (1u << e) : 0u;
   }
-  __syncthreads();
+  __syncthreads();  // sh.wcnt is rewritten by the caller's next step
+  return keep_mask;
+}
+
+// Writes the indices of the elements set in `mask` (K of them over the
+// workgroup) in ascending order to out[0..K).
+template <int E>
+__device__ void block_write_mask(uint32_t mask, int K, int32_t* out, SelectShared& sh) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  auto lanes_below = [&](unsigned long long bal) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+  };
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const unsigned long long bal = __ballot((keep_mask >> e) & 1u);
+    const unsigned long long bal = __ballot((mask >> e) & 1u);
     if (lane == 0) sh.wcnt[e * kSelWaves + wave] = __popcll(bal);
   }
   wcnt_scan(E * kSelWaves, sh);
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const bool kp = (keep_mask >> e) & 1u;
+    const bool kp = (mask >> e) & 1u;
     const int pos = sh.wcnt[e * kSelWaves + wave] + lanes_below(__ballot(kp));
     if (kp && pos < K) out[pos] = e * kSelThreads + tid;  // exactly K kept; the bound guards memory
   }
+}
+
+// Stable top-K: keep every element whose score is above the K-th largest and
+// the lowest-index elements equal to it, and write the kept indices in
+// ascending order to out[0..K).
+template <int E>
+__device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* out,
+                                 SelectShared& sh) {
+  const uint32_t mask = block_topk_mask<E>([&](int e) { return f2key(sc[e]); }, N, K, sh);
+  block_write_mask<E>(mask, K, out, sh);
 }
 
 }  // namespace trevs

@@ -547,6 +547,31 @@ __global__ __launch_bounds__(kSelThreads) void fuse_topk_kernel(SelArgs a) {
   block_topk_write<E>(sc, N, a.K, a.kept_idx + (size_t)b * a.K, sh);
 }
 
+// ---------------------------------------------------------------------------
+// Budget-split selection: one workgroup per sample.  The textual ratio read
+// as the share of the token budget given to textual relevance (the analysis
+// of Sec. 3): the K_t tokens with the highest s^t, then the K - K_t tokens
+// with the highest s^v among the rest (both stable: score descending, lower
+// index first), kept in ascending order.  Tokens already taken get the
+// smallest key in the second selection, below every finite score.
+// ---------------------------------------------------------------------------
+template <int E>
+__global__ __launch_bounds__(kSelThreads) void budget_topk_kernel(SelArgs a) {
+  __shared__ SelectShared sh;
+  const int b = blockIdx.x, tid = threadIdx.x, N = a.N;
+  float sv[E], st[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = min(e * kSelThreads + tid, N - 1);  // out-of-range elements are never valid below
+    sv[e] = a.sal[(size_t)b * N + i];
+    st[e] = a.rel[(size_t)b * N + i];
+  }
+  const uint32_t by_text = block_topk_mask<E>([&](int e) { return f2key(st[e]); }, N, a.K_t, sh);
+  const uint32_t by_sal = block_topk_mask<E>(
+      [&](int e) { return (by_text >> e) & 1u ? 0u : f2key(sv[e]); }, N, a.K - a.K_t, sh);
+  block_write_mask<E>(by_text | by_sal, a.K, a.kept_idx + (size_t)b * a.K, sh);
+}
+
 template <int E>
 __global__ __launch_bounds__(kSelThreads) void topk_kernel(const float* scores, int N, int K,
                                                            int32_t* out) {
@@ -641,6 +666,13 @@ hipError_t launch_norm_stats(const NormArgs& a, int B, hipStream_t s) {
 
 hipError_t launch_prellm_select(const SelArgs& a, int B, hipStream_t s) {
 #define CALL(E) hipLaunchKernelGGL(fuse_topk_kernel<E>, dim3(B), dim3(kSelThreads), 0, s, a)
+  TREVS_SELECT_SWITCH(select_e(a.N), CALL)
+#undef CALL
+  return hipGetLastError();
+}
+
+hipError_t launch_budget_select(const SelArgs& a, int B, hipStream_t s) {
+#define CALL(E) hipLaunchKernelGGL(budget_topk_kernel<E>, dim3(B), dim3(kSelThreads), 0, s, a)
   TREVS_SELECT_SWITCH(select_e(a.N), CALL)
 #undef CALL
   return hipGetLastError();

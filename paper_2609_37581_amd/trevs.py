@@ -42,7 +42,10 @@ class PrellmArgs(ctypes.Structure):
                 ("cls_logits", c_void_p), ("vis_feats", c_void_p), ("text_emb", c_void_p),
                 ("text_len", c_void_p), ("kept_idx", c_void_p), ("kept_feats", c_void_p),
                 ("score_out", c_void_p), ("sal_out", c_void_p), ("rel_out", c_void_p),
-                ("norm_stats", c_void_p), ("events", c_void_p)]
+                ("norm_stats", c_void_p), ("events", c_void_p), ("ratio_mode", c_int32)]
+
+
+RATIO_MODES = {"weights": 0, "budget": 1}
 
 
 class InllmArgs(ctypes.Structure):
@@ -145,7 +148,7 @@ class Prellm:
 
     def __init__(self, cls_logits, vis_feats, text_emb, text_len=None, *, k_keep, n_seg=1,
                  k_div=0, textual_ratio=0.5, tau_v=1.4, tau_t=1.0, lambda_=1.0, eps=1e-8,
-                 want_scores=False):
+                 want_scores=False, ratio_mode="weights"):
         dev = vis_feats.device
         _check(vis_feats, "vis_feats", dev, 3)
         dt = vis_feats.dtype
@@ -163,11 +166,15 @@ class Prellm:
         self.inputs = (cls_logits, vis_feats, text_emb, text_len)
         self.kept_idx = torch.empty((B, k_keep), dtype=torch.int32, device=dev)
         self.kept_feats = torch.empty((B, k_keep, d), dtype=dt, device=dev)
+        if ratio_mode not in RATIO_MODES:
+            raise ValueError(f"ratio_mode must be one of {sorted(RATIO_MODES)}")
+        budget = ratio_mode == "budget"
         if want_scores:
-            self.score = torch.empty((B, N), dtype=torch.float32, device=dev)
+            # the budget split ranks the raw scores: no fused score, no Med/MAD
+            self.score = None if budget else torch.empty((B, N), dtype=torch.float32, device=dev)
             self.sal = torch.empty((B, N), dtype=torch.float32, device=dev)
             self.rel = torch.empty((B, N), dtype=torch.float32, device=dev)
-            self.norm_stats = torch.empty((B, 4), dtype=torch.float32, device=dev)
+            self.norm_stats = None if budget else torch.empty((B, 4), dtype=torch.float32, device=dev)
         else:
             self.score = self.sal = self.rel = self.norm_stats = None
         a = PrellmArgs()
@@ -181,6 +188,7 @@ class Prellm:
         a.kept_idx, a.kept_feats = _ptr(self.kept_idx), _ptr(self.kept_feats)
         a.score_out, a.sal_out, a.rel_out = _ptr(self.score), _ptr(self.sal), _ptr(self.rel)
         a.norm_stats = _ptr(self.norm_stats)
+        a.ratio_mode = RATIO_MODES[ratio_mode]
         self.args = a
         ws = lib().trevs_prellm_workspace_size(ctypes.byref(a))
         if ws == 0:

@@ -40,7 +40,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_struct_mirror_sizes():
     L = trevs.lib()
-    assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 152
+    assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 160
     assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 192
 
 
@@ -85,6 +85,7 @@ def _inllm(**kw):
 def test_workspace_size_is_positive_for_valid_args():
     L = trevs.lib()
     assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm())) > 0
+    assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm(ratio_mode=1))) > 0
     assert L.trevs_inllm_workspace_size(ctypes.byref(_inllm())) > 0
 
 
@@ -95,6 +96,8 @@ def test_workspace_size_is_positive_for_valid_args():
     (dict(kept_feats=(1 << 40) + 8), 1), (dict(struct_size=10), 1), (dict(k_div=3), 2),
     (dict(N=40000, k_keep=10, n_seg=1), 2),
     (dict(kept_feats=(1 << 40) + (1 << 32) + 4096 * 64), 1),  # overlaps vis_feats
+    (dict(ratio_mode=2), 1), (dict(ratio_mode=1, score_out=(1 << 40) + (5 << 32)), 1),
+    (dict(ratio_mode=1, norm_stats=(1 << 40) + (5 << 32)), 1),
 ])
 def test_prellm_rejects_before_launch(bad, code):
     L = trevs.lib()

@@ -186,3 +186,51 @@ def test_stage1_rejects_bad_arguments_without_launching():
     with pytest.raises(trevs.TrevsError) as e:
         trevs.Prellm(cls, Z, T, k_keep=8, k_div=2)
     assert e.value.status == 2
+
+
+BUDGET_CASES = {
+    "llava15-b2-bf16-rho0.5": (WORKLOADS["llava15-b64-bf16"].with_(B=2), 0.5),
+    "sweep-b3-bf16-rho0.25": (WORKLOADS["sweep-llava15-b32-bf16"].with_(B=3), 0.25),
+    "tie-stress-bf16-rho0.75": (WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, tie_stress=True), 0.75),
+    "ragged-bf16-rho0.3": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=3, N=200, n_seg=2, d=4104, M_max=40, K1=37, n_sal=3, n_qm=5,
+        text_len=("uniform", 1, 40)), 0.3),
+    "rho0-f32": (WORKLOADS["llava15-b1-f32"], 0.0),
+    "rho1-f32": (WORKLOADS["llava15-b1-f32"], 1.0),
+    "qwen25vl-b1-bf16-rho0.5": (WORKLOADS["qwen25vl-b4-bf16"].with_(B=1), 0.5),
+}
+
+
+@pytest.mark.parametrize("name", list(BUDGET_CASES))
+def test_stage1_budget_split(name):
+    """Textual ratio as a budget split (Sec. 3 reading): scores against the
+    oracle, and the kept set exactly the oracle's budget split of the
+    kernel's own s^v and s^t (both selections are stable, so the set is
+    unique given the scores)."""
+    w, rho = BUDGET_CASES[name]
+    w = w.with_(rho=rho)
+    print(f"[stage1-budget] {name}: B={w.B} N={w.N} K1={w.K1} rho={rho}", flush=True)
+    inp = stage1_inputs(w)
+    cls = dev_tensor(inp["cls_logits"], w.dtype)
+    Z = dev_tensor(inp["vis_feats"], w.dtype)
+    T = dev_tensor(inp["text_emb"], w.dtype)
+    tl = torch.from_numpy(inp["text_len"]).cuda()
+    call = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, n_seg=w.n_seg, textual_ratio=rho,
+                        want_scores=True, ratio_mode="budget")
+    call()
+    torch.cuda.synchronize()
+    kept = call.kept_idx.cpu().numpy()
+    feats = host_bits(call.kept_feats)
+    sal, rel = call.sal.cpu().numpy(), call.rel.cpu().numpy()
+    rho32 = float(np.float32(rho))  # the library receives rho as float32
+    o = oracle.prellm(inp["cls_logits"], inp["vis_feats"], inp["text_emb"], inp["text_len"],
+                      w.dtype, n_seg=w.n_seg, k_keep=w.K1, rho=rho32, ratio_mode="budget")
+    assert_scores_close(sal, o["sal"], "s^v")
+    assert_scores_close(rel, o["rel"], "s^t")
+    for b in range(w.B):
+        want = oracle.budget_split_topk(sal[b].astype(np.float64), rel[b].astype(np.float64), w.K1, rho32)
+        assert np.array_equal(kept[b], want), b
+        assert np.array_equal(feats[b], inp["vis_feats"][b][kept[b]]), b
+        # against the oracle's own scores: equal outside the near-ties
+        agree = np.isin(kept[b], o["kept_idx"][b]).mean()
+        assert agree > 0.95, (b, agree)

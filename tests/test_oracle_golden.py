@@ -71,3 +71,10 @@ def test_compaction_rows():
     g = load("compaction.json")
     rows = oracle.compaction_rows(g["S"], g["P"], g["K1"], g["kept"])
     assert rows.tolist() == g["rows"]
+
+
+def test_budget_split():
+    g = load("budget_split.json")
+    for c in g["cases"]:
+        got = oracle.budget_split_topk(c["sv"], c["st"], c["k"], c["rho"])
+        assert got.tolist() == c["kept"], c

@@ -286,3 +286,49 @@ def test_bf16_decoding():
     t = torch.tensor([1.5, -3.25, 1e-3], dtype=torch.bfloat16)
     np.testing.assert_array_equal(oracle.to_f64(t.view(torch.uint16).numpy(), "bf16"),
                                   t.double().numpy())
+
+
+# ---------------------------------------------- textual ratio as a budget split
+@pytest.mark.parametrize("seed", range(4))
+def test_budget_split_extremes_and_invariants(seed):
+    """rho = 0 and rho = 1 reduce to one plain top-K; in general the kept set
+    holds the K_t best by s^t, the rest come from the top-k by s^v, and the
+    budget is spent exactly."""
+    rng = np.random.default_rng(seed)
+    n, k = 40, 13
+    sv = rng.integers(0, 9, size=n).astype(float)   # many ties
+    st = rng.integers(0, 9, size=n).astype(float)
+    assert oracle.budget_split_topk(sv, st, k, 0.0).tolist() == oracle.topk_ascending(sv, k).tolist()
+    assert oracle.budget_split_topk(sv, st, k, 1.0).tolist() == oracle.topk_ascending(st, k).tolist()
+    for rho in (0.2, 0.5, 0.8):
+        got = oracle.budget_split_topk(sv, st, k, rho)
+        k_t = int(np.floor(rho * k + 0.5))
+        assert got.size == k and np.all(np.diff(got) > 0)
+        by_text = set(oracle.topk_ascending(st, k_t).tolist())
+        assert by_text <= set(got.tolist())
+        assert set(got.tolist()) - by_text <= set(oracle.topk_ascending(sv, k).tolist())
+
+
+def test_budget_split_brute_force_small():
+    """Exhaustive check on tiny inputs: among all k-subsets, the kept set is the
+    one whose s^t part is the K_t first tokens in (s^t desc, index asc) order
+    and whose remaining part is lexicographically best in (s^v desc, index
+    asc) order among the subsets that contain that s^t part."""
+    rng = np.random.default_rng(7)
+    for _ in range(20):
+        n = int(rng.integers(2, 8))
+        k = int(rng.integers(1, n + 1))
+        rho = float(rng.choice([0.0, 0.3, 0.5, 0.75, 1.0]))
+        sv = rng.integers(0, 3, size=n).astype(float)
+        st = rng.integers(0, 3, size=n).astype(float)
+        k_t = int(np.floor(rho * k + 0.5))
+        first_t = sorted(range(n), key=lambda i: (-st[i], i))[:k_t]
+        best = None
+        for S in itertools.combinations(range(n), k):
+            if not set(first_t) <= set(S):
+                continue
+            rest = sorted((i for i in S if i not in first_t), key=lambda i: (-sv[i], i))
+            key = [(-sv[i], i) for i in rest]
+            if best is None or key < best[0]:
+                best = (key, list(S))
+        assert oracle.budget_split_topk(sv, st, k, rho).tolist() == best[1]
