@@ -61,7 +61,7 @@ def counter_traffic(workload):
     return float(vals["hbm_bytes_per_launch"])
 
 
-def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights"):
+def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights", k_div=0):
     """The CPU oracle as it stands, on single samples of the same workload,
     repeated until about budget_s seconds of work."""
     import oracle
@@ -76,7 +76,7 @@ def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights"):
         b = n % w.B
         oracle.prellm(s1["cls_logits"][b:b + 1], s1["vis_feats"][b:b + 1], s1["text_emb"][b:b + 1],
                       s1["text_len"][b:b + 1], w.dtype, n_seg=w.n_seg, k_keep=w.K1, rho=w.rho,
-                      ratio_mode=ratio_mode)
+                      ratio_mode=ratio_mode, k_div=k_div)
         oracle.inllm(s2["q"][b:b + 1], s2["k"][b:b + 1], s2["v"][b:b + 1], s2["hidden"][b:b + 1],
                      s2["pos"][:, b:b + 1], s2["text_len"][b:b + 1], w.dtype, P=w.P, K1=w.K1,
                      n_keep=w.n_keep, k_keep=w.K2, scale=1.0 / math.sqrt(w.d_h))
@@ -97,6 +97,8 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--k-div", type=int, default=0,
+                    help="farthest-point diversity tokens K_d within K1 (default 0: all pivots)")
     ap.add_argument("--ratio-mode", default="weights", choices=["weights", "budget"],
                     help="textual ratio as Eq. (7) branch weights (default) or as a budget split")
     args = ap.parse_args()
@@ -126,7 +128,7 @@ def main():
     q, k, v, hid, pos = (to_dev(s2[x]) for x in ("q", "k", "v", "hidden", "pos"))
     tl2 = to_dev(s2["text_len"])
     pre = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, n_seg=w.n_seg, textual_ratio=w.rho,
-                       ratio_mode=args.ratio_mode)
+                       ratio_mode=args.ratio_mode, k_div=args.k_div)
     inl = trevs.Inllm(q, k, v, hid, pos, tl2, P=w.P, K_in=w.K1, n_keep_heads=w.n_keep,
                       k_keep=w.K2)
     stream = torch.cuda.current_stream()
@@ -212,7 +214,7 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "ratio_mode": args.ratio_mode, "B": w.B, "N": w.N, "d": w.d, "M_max": w.M_max,
+        "config": {"workload": w.name, "ratio_mode": args.ratio_mode, "k_div": args.k_div, "B": w.B, "N": w.N, "d": w.d, "M_max": w.M_max,
                    "K1": w.K1, "K2": w.K2, "H_q": w.H_q, "H_kv": w.H_kv, "d_head": w.d_h,
                    "D": w.D, "n_keep_heads": w.n_keep, "P": w.P, "S": w.S},
         "roofline": {"bound": "hbm", "kernel": "prellm.relevance", "achieved": achieved,
@@ -227,7 +229,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(w, s1, s2, args.cpu_seconds, args.ratio_mode)
+        result["cpu_baseline"] = cpu_baseline(w, s1, s2, args.cpu_seconds, args.ratio_mode, args.k_div)
     print(json.dumps(result), flush=True)
 
 

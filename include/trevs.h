@@ -57,7 +57,7 @@ typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
 
 /* Implementation limits (TREVS_ERR_UNSUPPORTED beyond them). */
 #define TREVS_MAX_SELECT_N 32768 /* tokens ranked per sample by one top-K */
-#define TREVS_PRELLM_NUM_KERNELS 5 /* prep, relevance, robust stats, fuse+top-K, gather */
+#define TREVS_PRELLM_NUM_KERNELS 5 /* prep, relevance, robust stats, fuse+top-K (+ diversity set), gather */
 #define TREVS_INLLM_NUM_KERNELS 5  /* t2v stats, head variance, head set+token score, top-K, compaction */
 
 /* ------------------------------------------------------------------------
@@ -76,6 +76,12 @@ typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
  *            rho = 0.5 is Eq. (7) exactly, rho = 0 is [CLS]-only saliency).
  *   kept_idx[b]   = TopK(s, k_keep) in ascending order
  *   kept_feats[b] = vis_feats[b, kept_idx[b], :]  (bit copy)
+ * With k_div = K_d > 0 the top-K above keeps K_r = k_keep - K_d pivots, and
+ * K_d more tokens are added by farthest point sampling (context
+ * preservation, Sec. 4.1 after Eq. (7)): one at a time, the token outside
+ * the selected set whose cosine distance 1 - zbar_i . zbar_j to its nearest
+ * selected token is largest (ties to the lower index).  This forms the Gram
+ * matrix Z Z^T of every sample in the workspace (B*N*N floats).
  * With ratio_mode = TREVS_RATIO_BUDGET the textual ratio is instead the
  * share of the token budget given to textual relevance (the reading of the
  * preliminary analysis, Sec. 3): K_t = floor(rho * k_keep + 1/2) tokens with
@@ -97,7 +103,7 @@ typedef struct trevs_prellm_args {
   int32_t d;                 /* projected width d'; d * elem_size % 16 == 0 */
   int32_t M_max;             /* padded text rows, >= 1 */
   int32_t k_keep;            /* K_1 = K_r + K_d, 1..N */
-  int32_t k_div;             /* K_d (farthest-point diversity set); must be 0 */
+  int32_t k_div;             /* K_d farthest-point diversity tokens, 0..k_keep-1 */
   float textual_ratio;       /* rho in [0, 1]; 0.5 reproduces Eq. (7) */
   float tau_v, tau_t;        /* temperatures > 0 (paper: 1.4, 1.0) */
   float lambda_;             /* consistency reward weight >= 0 (paper: 1.0) */
@@ -115,6 +121,7 @@ typedef struct trevs_prellm_args {
   float* norm_stats;         /* OPTIONAL OUT [B,4] Med(s^v), MAD(s^v), Med(s^t), MAD(s^t) */
   void* const* events;       /* OPTIONAL [2*TREVS_PRELLM_NUM_KERNELS] hipEvent_t */
   int32_t ratio_mode;        /* trevs_ratio_mode */
+  int32_t* div_idx;          /* OPTIONAL OUT [B,k_div] diversity tokens in pick order */
 } trevs_prellm_args;
 
 /* ------------------------------------------------------------------------

@@ -229,7 +229,7 @@ def prellm(cls_logits, Z, T, text_len, dtype, *, n_seg=1, k_keep, k_div=0,
     B = cls_logits.shape[0]
     M_max = T.shape[1]
     out = {k: [] for k in ("sal", "rel", "score", "kept_idx", "kept_feats",
-                           "med_v", "mad_v", "med_t", "mad_t")}
+                           "med_v", "mad_v", "med_t", "mad_t", "pivots", "diverse")}
     for b in range(B):
         mb = M_max if text_len is None else int(text_len[b])
         if not 1 <= mb <= M_max:
@@ -239,7 +239,7 @@ def prellm(cls_logits, Z, T, text_len, dtype, *, n_seg=1, k_keep, k_div=0,
                           k_div=k_div, rho=rho, tau_v=tau_v, tau_t=tau_t,
                           lam=lam, eps=eps, ratio_mode=ratio_mode)
         for key in ("sal", "rel", "score", "kept_idx", "med_v", "mad_v",
-                    "med_t", "mad_t"):
+                    "med_t", "mad_t", "pivots", "diverse"):
             out[key].append(r[key])
         out["kept_feats"].append(np.asarray(Z[b])[r["kept_idx"]])
     return {k: np.stack(v) if isinstance(v[0], np.ndarray) else np.array(v)

@@ -52,7 +52,7 @@ trevs_status record(void* const* events, int slot, hipStream_t s) {
 
 // ------------------------------------------------------------------ stage 1
 struct PrellmLayout {
-  size_t row_stats, inv_tnorm, sal, rel, stats, total;
+  size_t row_stats, inv_tnorm, sal, rel, stats, pivots, gram, dist, inv_norm, total;
 };
 
 trevs_status validate_prellm(const trevs_prellm_args* a) {
@@ -91,11 +91,12 @@ trevs_status validate_prellm(const trevs_prellm_args* a) {
                       {a->score_out, a->score_out ? B * N * 4 : 0},
                       {a->sal_out, a->sal_out ? B * N * 4 : 0},
                       {a->rel_out, a->rel_out ? B * N * 4 : 0},
-                      {a->norm_stats, a->norm_stats ? B * 16 : 0}};
-  if (any_overlap(out, 6, in, 4)) return TREVS_ERR_INVALID_ARG;
+                      {a->norm_stats, a->norm_stats ? B * 16 : 0},
+                      {a->div_idx, a->div_idx ? B * a->k_div * 4 : 0}};
+  if (any_overlap(out, 7, in, 4)) return TREVS_ERR_INVALID_ARG;
+  if (!aligned(a->div_idx, 4)) return TREVS_ERR_INVALID_ARG;
   if (a->ratio_mode != TREVS_RATIO_WEIGHTS && a->ratio_mode != TREVS_RATIO_BUDGET) return TREVS_ERR_INVALID_ARG;
   if (a->ratio_mode == TREVS_RATIO_BUDGET && (a->score_out || a->norm_stats)) return TREVS_ERR_INVALID_ARG;
-  if (a->k_div > 0) return TREVS_ERR_UNSUPPORTED;
   if (a->N > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
   return TREVS_OK;
 }
@@ -119,6 +120,17 @@ PrellmLayout prellm_layout(const trevs_prellm_args* a) {
   off = align_up(off + (size_t)a->B * a->N * sizeof(float));
   L.stats = off;
   off = align_up(off + (size_t)a->B * 4 * sizeof(float));
+  L.pivots = L.gram = L.dist = L.inv_norm = off;
+  if (a->k_div > 0) {  // farthest point sampling: pivot list, Gram matrices, distances
+    L.pivots = off;
+    off = align_up(off + (size_t)a->B * (a->k_keep - a->k_div) * sizeof(int32_t));
+    L.gram = off;
+    off = align_up(off + (size_t)a->B * a->N * a->N * sizeof(float));
+    L.dist = off;
+    off = align_up(off + (size_t)a->B * a->N * sizeof(float));
+    L.inv_norm = off;
+    off = align_up(off + (size_t)a->B * a->N * sizeof(float));
+  }
   L.total = off;
   return L;
 }
@@ -342,13 +354,37 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   sa.eps = a->eps;
   sa.score_out = a->score_out;
   sa.norm_stats = a->norm_stats;
-  sa.kept_idx = a->kept_idx;
-  sa.K_t = budget_text_count(a->textual_ratio, a->k_keep);
+  // with a diversity set the top-K keeps the K_r pivots, and farthest point
+  // sampling adds the other K_d tokens and writes the kept list
+  const int K_r = a->k_keep - a->k_div;
+  int32_t* pivots = reinterpret_cast<int32_t*>(w + L.pivots);
+  sa.K = K_r;
+  sa.kept_idx = a->k_div > 0 ? pivots : a->kept_idx;
+  sa.K_t = budget_text_count(a->textual_ratio, K_r);
   TREVS_TRY(record(a->events, 6, s));
   if (budget)
     TREVS_HIP(launch_budget_select(sa, a->B, s));
   else
     TREVS_HIP(launch_prellm_select(sa, a->B, s));
+  if (a->k_div > 0) {
+    GramArgs ga;
+    ga.Z = a->vis_feats;
+    ga.N = a->N;
+    ga.row_bytes = a->d * e;
+    ga.n_tiles = (a->N + 127) / 128;
+    ga.G = reinterpret_cast<float*>(w + L.gram);
+    FpsArgs fa;
+    fa.G = ga.G;
+    fa.pivots = pivots;
+    fa.N = a->N;
+    fa.K_r = K_r;
+    fa.K_d = a->k_div;
+    fa.dist = reinterpret_cast<float*>(w + L.dist);
+    fa.inv_norm = reinterpret_cast<float*>(w + L.inv_norm);
+    fa.kept_idx = a->kept_idx;
+    fa.div_idx = a->div_idx;
+    TREVS_HIP(launch_fps(fa, ga, a->dtype, a->B, s));
+  }
   TREVS_TRY(record(a->events, 7, s));
 
   GatherArgs ga;

@@ -1,0 +1,253 @@
+// Context preservation by farthest point sampling (Sec. 4.1, after Eq. (7)):
+// K_d tokens are added one at a time to the pivot set, each the candidate
+// whose cosine distance 1 - zbar_i . zbar_j to the nearest already-selected
+// token is largest (ties to the lower index).
+//
+// The picks are sequential, and every pick needs the distances of all
+// candidates to one more token.  Instead of re-reading Z for each pick, the
+// Gram matrix G = Z Z^T of the sample is formed once on the matrix cores;
+// a pick then reads one row of G (N floats).  ||z_i||^2 is its diagonal.
+#include "common.hpp"
+#include "kernels.hpp"
+#include "select.hpp"
+
+namespace trevs {
+
+// ---------------------------------------------------------------------------
+// Gram matrix.  A workgroup of 4 waves computes a 128x128 tile of G[b]
+// (rows j of the tile's first operand, columns i of the second), streaming
+// the feature dimension in 128-byte slabs: each thread loads its share of
+// both slabs with coalesced 16-byte loads (8 lanes per 128-byte row
+// segment) into a ring of two register buffers, writes them to one of two
+// LDS buffers (rows XOR-swizzled by 16-byte chunk), and the waves multiply
+// on the matrix cores, each a 64x64 block.  Bytes past a row's end (a
+// partial last slab) load as zero.
+// ---------------------------------------------------------------------------
+constexpr int kGramTile = 128;
+constexpr int kGramThreads = 256;
+
+__device__ __forceinline__ int gram_swizzle(int r, int c) { return c ^ ((r >> 1) & 7); }
+
+template <class In>
+__global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
+  constexpr int T = kGramTile;
+  constexpr int SLAB = T * 128;                  // bytes of one operand slab
+  constexpr int VPT = SLAB / 16 / kGramThreads;  // vectors per thread per operand
+  __shared__ __attribute__((aligned(1024))) uint8_t l0[2 * SLAB], l1[2 * SLAB];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  const int nT = a.n_tiles;
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = lin / (nT * nT), t2 = lin - b * nT * nT;
+  const int tj = t2 / nT, ti = t2 - tj * nT;
+  const int N = a.N, rb = a.row_bytes;
+  const int n_slabs = (rb + 127) / 128;
+  const uint8_t* zb = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
+  const int cr = tid >> 3, cc = tid & 7;
+  const uint8_t* src[2 * VPT];  // row starts (rows past N re-read row N - 1)
+#pragma unroll
+  for (int k = 0; k < VPT; ++k) {
+    const int r = cr + (kGramThreads / 8) * k;
+    src[k] = zb + (size_t)min(tj * T + r, N - 1) * rb;
+    src[VPT + k] = zb + (size_t)min(ti * T + r, N - 1) * rb;
+  }
+  const int sdst = cr * 128 + gram_swizzle(cr, cc) * 16;  // rows 32 apart share the swizzle
+  u32x4 g[2][2 * VPT];
+  // chunk cc of slab s; a chunk past the row's end reads the row's first
+  // chunk (in bounds) and is replaced by zero; the padding steps past the
+  // last slab re-read it and are never multiplied
+  auto load = [&](int s, u32x4 (&dst)[2 * VPT]) {
+    const int off = min(s, n_slabs - 1) * 128 + cc * 16;
+    const bool in_row = off < rb;
+#pragma unroll
+    for (int k = 0; k < 2 * VPT; ++k) {
+      const u32x4 v = ldg16(src[k] + (in_row ? off : 0));
+      dst[k] = in_row ? v : zero4();
+    }
+  };
+  auto store = [&](uint8_t* st, const u32x4 (&v)[2 * VPT]) {
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) {
+      *reinterpret_cast<u32x4*>(st + sdst + k * (kGramThreads / 8) * 128) = v[k];
+      *reinterpret_cast<u32x4*>(st + SLAB + sdst + k * (kGramThreads / 8) * 128) = v[VPT + k];
+    }
+  };
+  const int wj = wave >> 1, wi = wave & 1;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
+  auto frag = [&](const uint8_t* base, int row, u32x4 (&f)[4]) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      f[q] = *reinterpret_cast<const u32x4*>(base + row * 128 + gram_swizzle(row, 4 * half + q) * 16);
+  };
+  auto compute = [&](const uint8_t* st) {
+    u32x4 fa[2][4], fb[2][4];
+#pragma unroll
+    for (int m = 0; m < 2; ++m) frag(st, wj * 64 + m * 32 + col, fa[m]);
+#pragma unroll
+    for (int n = 0; n < 2; ++n) frag(st + SLAB, wi * 64 + n * 32 + col, fb[n]);
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int n = 0; n < 2; ++n) acc[m][n] = mfma_frag(fa[m], fb[n], acc[m][n], In{});
+  };
+  load(0, g[0]);
+  load(1, g[1]);
+  const int n_iter = (n_slabs + 1) / 2;
+  for (int it = 0; it < n_iter; ++it) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int s = 2 * it + c;
+      uint8_t* st = c ? l1 : l0;
+      // buffer c was last read at step s - 2, before every wave passed the
+      // barrier of step s - 1
+      store(st, g[c]);
+      load(s + 2, g[c]);
+      __syncthreads();
+      if (s < n_slabs) compute(st);
+    }
+  }
+  // output: register r of block (m, n) is row wj*64 + m*32 + mfma_row(r),
+  // column wi*64 + n*32 + col of the tile
+  float* gb = a.G + (size_t)b * N * N;
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int n = 0; n < 2; ++n) {
+      const int i = ti * T + wi * 64 + n * 32 + col;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = tj * T + wj * 64 + m * 32 + mfma_row(r, half);
+        if (i < N && j < N) gb[(size_t)j * N + i] = acc[m][n][r];
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Initial distances: for every token i, 1 - max over the pivots j of
+// cos(z_i, z_j) = G_ij / (||z_i|| ||z_j||) (norms floored at 1e-12), and
+// 1/||z_i|| for the picks.
+// ---------------------------------------------------------------------------
+constexpr int kFpsInitThreads = 256;
+
+__global__ __launch_bounds__(kFpsInitThreads) void fps_init_kernel(FpsArgs a) {
+  const int b = blockIdx.y, i = blockIdx.x * kFpsInitThreads + threadIdx.x, N = a.N;
+  if (i >= N) return;
+  const float* gb = a.G + (size_t)b * N * N;
+  const float iz = 1.f / fmaxf(sqrtf(fmaxf(gb[(size_t)i * N + i], 0.f)), 1e-12f);
+  const int32_t* piv = a.pivots + (size_t)b * a.K_r;
+  float mx = -INFINITY;
+  for (int p = 0; p < a.K_r; ++p) {
+    const int j = piv[p];
+    const float izj = 1.f / fmaxf(sqrtf(fmaxf(gb[(size_t)j * N + j], 0.f)), 1e-12f);
+    mx = fmaxf(mx, gb[(size_t)j * N + i] * iz * izj);
+  }
+  a.dist[(size_t)b * N + i] = 1.f - mx;
+  a.inv_norm[(size_t)b * N + i] = iz;
+}
+
+// ---------------------------------------------------------------------------
+// The picks: one workgroup per sample walks the K_d sequential steps with
+// the distances of its tokens in registers (element e*1024 + t of thread t,
+// as in the selection kernels).  Each step reduces (distance desc, index
+// asc) over the unselected tokens, marks the winner, and lowers every
+// distance with the winner's row of G.  The selected set (pivots and picks)
+// is then written in ascending order.
+// ---------------------------------------------------------------------------
+template <int E>
+__global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
+  __shared__ SelectShared sh;
+  __shared__ float wv[2][kSelWaves];
+  __shared__ int wi[2][kSelWaves];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int N = a.N, K_r = a.K_r;
+  const int32_t* piv = a.pivots + (size_t)b * K_r;
+  const float* gb = a.G + (size_t)b * N * N;
+  auto valid = [&](int e) { return e * kSelThreads + tid < N; };
+  float dist[E], iz[E];
+  uint32_t sel = 0u;  // bit e: element e is selected (a pivot or a pick)
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = min(e * kSelThreads + tid, N - 1);
+    dist[e] = a.dist[(size_t)b * N + i];
+    iz[e] = a.inv_norm[(size_t)b * N + i];
+    // pivot membership by binary search in the ascending pivot list
+    int lo = 0, hi = K_r;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (piv[mid] < i) lo = mid + 1; else hi = mid;
+    }
+    if (valid(e) && lo < K_r && piv[lo] == i) sel |= 1u << e;
+  }
+  for (int t = 0; t < a.K_d; ++t) {
+    float v = -INFINITY;
+    int idx = 0x7fffffff;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (valid(e) && !((sel >> e) & 1u) && dist[e] > v) {  // ascending e: the lower index wins ties
+        v = dist[e];
+        idx = e * kSelThreads + tid;
+      }
+    const float vm = wave_max(v);
+    const uint32_t im = wave_min_u32(v == vm ? (uint32_t)idx : 0xffffffffu);
+    const int buf = t & 1;  // alternate slots: one barrier per step suffices
+    if (lane == 0) {
+      wv[buf][wave] = vm;
+      wi[buf][wave] = (int)im;
+    }
+    __syncthreads();
+    float bv = wv[buf][0];
+    int w = wi[buf][0];
+#pragma unroll
+    for (int k = 1; k < kSelWaves; ++k) {
+      const float v2 = wv[buf][k];
+      const int i2 = wi[buf][k];
+      if (v2 > bv || (v2 == bv && i2 < w)) {
+        bv = v2;
+        w = i2;
+      }
+    }
+    w = min(max(w, 0), N - 1);  // K_r + K_d <= N leaves a candidate at every step
+    if (tid == 0 && a.div_idx) a.div_idx[(size_t)b * a.K_d + t] = w;
+    if ((w & (kSelThreads - 1)) == tid) sel |= 1u << (w / kSelThreads);
+    const float* row = gb + (size_t)w * N;
+    const float izw = a.inv_norm[(size_t)b * N + w];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float gi = row[min(e * kSelThreads + tid, N - 1)];
+      if (valid(e) && !((sel >> e) & 1u)) dist[e] = fminf(dist[e], 1.f - gi * iz[e] * izw);
+    }
+  }
+  block_write_mask<E>(sel, K_r + a.K_d, a.kept_idx + (size_t)b * (K_r + a.K_d), sh);
+}
+
+// ---------------------------------------------------------------- launchers
+hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hipStream_t s) {
+  const dim3 ggrid(B * g.n_tiles * g.n_tiles);
+  if (dtype == 1)
+    hipLaunchKernelGGL(gram_kernel<BF16>, ggrid, dim3(kGramThreads), 0, s, g);
+  else
+    hipLaunchKernelGGL(gram_kernel<F32>, ggrid, dim3(kGramThreads), 0, s, g);
+  hipLaunchKernelGGL(fps_init_kernel, dim3((f.N + kFpsInitThreads - 1) / kFpsInitThreads, B),
+                     dim3(kFpsInitThreads), 0, s, f);
+  const int E = select_e(f.N);
+#define CALL(E_) hipLaunchKernelGGL(fps_pick_kernel<E_>, dim3(B), dim3(kSelThreads), 0, s, f)
+  switch (E) {
+    case 1: CALL(1); break;
+    case 2: CALL(2); break;
+    case 4: CALL(4); break;
+    case 8: CALL(8); break;
+    case 16: CALL(16); break;
+    case 32: CALL(32); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef CALL
+  return hipGetLastError();
+}
+
+}  // namespace trevs

@@ -84,6 +84,24 @@ struct ScoreArgs {
   float* p;                  // [B,K_in]
 };
 
+// ---------------------------------------------------------------- diversity set
+struct GramArgs {
+  const void* Z;             // [B,N,d]
+  int N, row_bytes, n_tiles; // n_tiles = ceil(N / 128)
+  float* G;                  // [B,N,N] fp32 dot products z_j . z_i
+};
+struct FpsArgs {
+  const float* G;            // [B,N,N]
+  const int32_t* pivots;     // [B,K_r] ascending
+  int N, K_r, K_d;
+  float* dist;               // [B,N] work: distance to the selected set
+  float* inv_norm;           // [B,N] work: 1 / ||z_i||
+  int32_t* kept_idx;         // [B,K_r+K_d] ascending
+  int32_t* div_idx;          // [B,K_d] picks in pick order, or null
+};
+// Gram matrix, initial distances and the K_d sequential picks.
+hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hipStream_t s);
+
 // ---------------------------------------------------------------- gather
 constexpr int kGatherMaxTensors = 4;
 struct GatherTensor {
@@ -104,6 +122,14 @@ struct GatherArgs {
 constexpr int kGatherRowsPerBlock = 4;  // one row per wave
 constexpr int kGatherThreads = 256;
 constexpr int kGatherBatch = 8;  // 16-byte loads in flight per lane
+
+// Elements per thread of a 1024-thread selection workgroup over N values
+// (a power of two, the template argument of the selection kernels).
+inline int select_e(int N) {
+  int e = 1;
+  while (e * 1024 < N) e <<= 1;
+  return e;
+}
 
 hipError_t launch_prep(const PrepArgs& a, int dtype, hipStream_t s);
 hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s);

@@ -640,11 +640,6 @@ hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s) 
   return hipGetLastError();
 }
 
-static int select_e(int N) {
-  int e = 1;
-  while (e * kSelThreads < N) e <<= 1;
-  return e;
-}
 
 #define TREVS_SELECT_SWITCH(E_, CALL)   \
   switch (E_) {                         \

@@ -42,7 +42,8 @@ class PrellmArgs(ctypes.Structure):
                 ("cls_logits", c_void_p), ("vis_feats", c_void_p), ("text_emb", c_void_p),
                 ("text_len", c_void_p), ("kept_idx", c_void_p), ("kept_feats", c_void_p),
                 ("score_out", c_void_p), ("sal_out", c_void_p), ("rel_out", c_void_p),
-                ("norm_stats", c_void_p), ("events", c_void_p), ("ratio_mode", c_int32)]
+                ("norm_stats", c_void_p), ("events", c_void_p), ("ratio_mode", c_int32),
+                ("div_idx", c_void_p)]
 
 
 RATIO_MODES = {"weights": 0, "budget": 1}
@@ -165,6 +166,8 @@ class Prellm:
             raise ValueError("text_len must be [B]")
         self.inputs = (cls_logits, vis_feats, text_emb, text_len)
         self.kept_idx = torch.empty((B, k_keep), dtype=torch.int32, device=dev)
+        # farthest-point diversity tokens in pick order (k_div > 0)
+        self.div_idx = torch.empty((B, k_div), dtype=torch.int32, device=dev) if k_div > 0 else None
         self.kept_feats = torch.empty((B, k_keep, d), dtype=dt, device=dev)
         if ratio_mode not in RATIO_MODES:
             raise ValueError(f"ratio_mode must be one of {sorted(RATIO_MODES)}")
@@ -189,6 +192,7 @@ class Prellm:
         a.score_out, a.sal_out, a.rel_out = _ptr(self.score), _ptr(self.sal), _ptr(self.rel)
         a.norm_stats = _ptr(self.norm_stats)
         a.ratio_mode = RATIO_MODES[ratio_mode]
+        a.div_idx = _ptr(self.div_idx)
         self.args = a
         ws = lib().trevs_prellm_workspace_size(ctypes.byref(a))
         if ws == 0:

@@ -40,7 +40,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_struct_mirror_sizes():
     L = trevs.lib()
-    assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 160
+    assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 168
     assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 192
 
 
@@ -86,6 +86,9 @@ def test_workspace_size_is_positive_for_valid_args():
     L = trevs.lib()
     assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm())) > 0
     assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm(ratio_mode=1))) > 0
+    # the diversity set adds the Gram matrices of the batch: B * N * N floats
+    plain = L.trevs_prellm_workspace_size(ctypes.byref(_prellm()))
+    assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm(k_div=48))) >= plain + 2 * 576 * 576 * 4
     assert L.trevs_inllm_workspace_size(ctypes.byref(_inllm())) > 0
 
 
@@ -93,7 +96,8 @@ def test_workspace_size_is_positive_for_valid_args():
     (dict(k_keep=0), 1), (dict(k_keep=577), 1), (dict(n_seg=5), 1), (dict(d=4095), 1),
     (dict(textual_ratio=-0.1), 1), (dict(textual_ratio=float("nan")), 1), (dict(tau_v=0.0), 1),
     (dict(eps=-1.0), 1), (dict(dtype=7), 1), (dict(vis_feats=None), 1),
-    (dict(kept_feats=(1 << 40) + 8), 1), (dict(struct_size=10), 1), (dict(k_div=3), 2),
+    (dict(kept_feats=(1 << 40) + 8), 1), (dict(struct_size=10), 1), (dict(k_div=192), 1),
+    (dict(k_div=-1), 1), (dict(k_div=3, div_idx=(1 << 40) + (5 << 32) + 2), 1),
     (dict(N=40000, k_keep=10, n_seg=1), 2),
     (dict(kept_feats=(1 << 40) + (1 << 32) + 4096 * 64), 1),  # overlaps vis_feats
     (dict(ratio_mode=2), 1), (dict(ratio_mode=1, score_out=(1 << 40) + (5 << 32)), 1),

@@ -234,3 +234,69 @@ def test_stage1_budget_split(name):
         # against the oracle's own scores: equal outside the near-ties
         agree = np.isin(kept[b], o["kept_idx"][b]).mean()
         assert agree > 0.95, (b, agree)
+
+
+# ------------------------------------------------------------- diversity set
+def _fps_distances(Z64, selected):
+    """Distance of every token to its nearest selected token, from the
+    oracle's normalised features (float64)."""
+    zbar = oracle.l2_normalise_rows(Z64)
+    return (1.0 - zbar @ zbar[np.asarray(selected)].T).min(axis=1)
+
+
+FPS_CASES = {
+    "llava15-b2-bf16": (WORKLOADS["llava15-b64-bf16"].with_(B=2), 48),
+    "llava15-b1-f32": (WORKLOADS["llava15-b1-f32"], 48),
+    # rows with a partial 128-byte slab, N not a multiple of the 128-row tile
+    "ragged-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=3, N=200, n_seg=2, d=4104, M_max=40, K1=37, n_sal=3, n_qm=5,
+        text_len=("uniform", 1, 40)), 9),
+    "tie-stress-bf16": (WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, tie_stress=True), 30),
+    "one-pivot-bf16": (WORKLOADS["llava15-b64-bf16"].with_(B=1, K1=20), 19),
+}
+
+
+@pytest.mark.parametrize("name", list(FPS_CASES))
+def test_stage1_diversity_set(name):
+    """Context preservation by farthest point sampling (Sec. 4.1, after Eq.
+    (7)).  The pivots are the exact top-K_r of the kernel's own fused score;
+    the picks follow the oracle's sequential rule from the same pivots, step
+    for step, unless a step is a genuine near-tie (the two candidates' oracle
+    distances within 1e-5), after which the sequences may legitimately part;
+    the kept list is the ascending union and the gather is bit-exact."""
+    w, k_div = FPS_CASES[name]
+    print(f"[stage1-fps] {name}: B={w.B} N={w.N} K1={w.K1} K_d={k_div}", flush=True)
+    inp = stage1_inputs(w)
+    cls = dev_tensor(inp["cls_logits"], w.dtype)
+    Z = dev_tensor(inp["vis_feats"], w.dtype)
+    T = dev_tensor(inp["text_emb"], w.dtype)
+    tl = torch.from_numpy(inp["text_len"]).cuda()
+    call = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, k_div=k_div, n_seg=w.n_seg,
+                        textual_ratio=w.rho, want_scores=True)
+    call()
+    torch.cuda.synchronize()
+    kept = call.kept_idx.cpu().numpy()
+    picks = call.div_idx.cpu().numpy()
+    feats = host_bits(call.kept_feats)
+    score = call.score.cpu().numpy()
+    K_r = w.K1 - k_div
+    o = run_oracle(inp, w, k_div=k_div)
+    assert_scores_close(score, o["score"], "s")
+    for b in range(w.B):
+        pivots = np.setdiff1d(kept[b], picks[b])
+        assert pivots.size == K_r and np.unique(picks[b]).size == k_div, b
+        assert np.array_equal(pivots, oracle.topk_ascending(score[b].astype(np.float64), K_r)), b
+        assert np.array_equal(kept[b], np.sort(np.concatenate([pivots, picks[b]]))), b
+        assert np.array_equal(feats[b], inp["vis_feats"][b][kept[b]]), b
+        Z64 = oracle.to_f64(inp["vis_feats"][b], w.dtype)
+        want = oracle.farthest_point_sampling(Z64, pivots, k_div)
+        sel = list(pivots)
+        for t in range(k_div):
+            if picks[b][t] == want[t]:
+                sel.append(int(picks[b][t]))
+                continue
+            d = _fps_distances(Z64, sel)
+            assert picks[b][t] not in sel, (b, t)
+            gap = abs(d[picks[b][t]] - d[want[t]])
+            assert gap <= 1e-5, (b, t, picks[b][t], want[t], gap)
+            break  # a near-tie: later picks may legitimately differ
