@@ -122,6 +122,7 @@ struct GatherArgs {
 constexpr int kGatherRowsPerBlock = 4;  // one row per wave
 constexpr int kGatherThreads = 256;
 constexpr int kGatherBatch = 8;  // 16-byte loads in flight per lane
+constexpr int kGatherShortRows = 8;  // rows of at most 1 KB per wave
 
 // Elements per thread of a 1024-thread selection workgroup over N values
 // (a power of two, the template argument of the selection kernels).

@@ -184,8 +184,8 @@ def test_stage1_rejects_bad_arguments_without_launching():
         trevs.Prellm(cls, Z, T, k_keep=8, textual_ratio=1.5)
     assert e.value.status == 1
     with pytest.raises(trevs.TrevsError) as e:
-        trevs.Prellm(cls, Z, T, k_keep=8, k_div=2)
-    assert e.value.status == 2
+        trevs.Prellm(cls, Z, T, k_keep=8, k_div=8)
+    assert e.value.status == 1
 
 
 BUDGET_CASES = {
