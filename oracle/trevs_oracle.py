@@ -21,6 +21,9 @@ Stage 2 (Sec. 4.2, "Query-Driven Visual Token Compression"):
     Eq. (8)  per-head text->vision attention variance u_h; top heads H*
     Eq. (9)  token score p_i = max over text rows of the H*-mean attention,
              then Top-K_2 and compaction of the sequence for later layers.
+Diagnostics (Sec. 3, preliminary analysis):
+    Eq. (1)  text sensitivity TS_h of a head between two questions
+    the Spearman correlation of s^v and s^t inside the top-K saliency set
 
 Readings where the paper is silent (each also listed in the design notes):
   * median = LOWER median, the order statistic of 0-based rank floor((n-1)/2);
@@ -41,6 +44,10 @@ Readings where the paper is silent (each also listed in the design notes):
     the full-sequence softmax restricted to the visual columns.
   * compaction keeps the prefix rows, the K_2 selected visual rows (ascending)
     and the text rows, and copies the original position ids unchanged.
+  * Eq. (1) (analysis of Sec. 3): a head's visual-token attention
+    distribution for a question is the mean of its text->vision attention
+    rows over the valid text rows; the Spearman correlation of Sec. 3 uses
+    average ranks for ties and is NaN when either ranking is constant.
 """
 
 import math
@@ -350,6 +357,102 @@ def inllm(q, k, v, hidden, pos, text_len, dtype, *, P, K1, n_keep, k_keep,
     out["v_out"] = np.asarray(v)[bidx, rows]
     out["pos_out"] = np.asarray(pos)[:, bidx, rows]
     return out
+
+
+# ----------------------------------------------------------------------------
+# Diagnostic quantities of the preliminary analysis (Sec. 3)
+# ----------------------------------------------------------------------------
+
+
+def visual_profile(A):
+    """The attention distribution of each head over the visual tokens for one
+    question (the s_h of Eq. (1)), read as the mean of A_{T->V}[h, q, :] over
+    the question's valid text rows.  A [H_q, T_b, K_1] -> [H_q, K_1]."""
+    return A.mean(axis=1)
+
+
+def text_sensitivity(s1, s2):
+    """Eq. (1): TS_h = 1 - cos(s_h^(1), s_h^(2)) between a head's visual
+    profiles under two questions.  s1, s2 [H_q, K_1] -> [H_q]."""
+    dot = (s1 * s2).sum(axis=-1)
+    return 1.0 - dot / (np.linalg.norm(s1, axis=-1) * np.linalg.norm(s2, axis=-1))
+
+
+def sensitivity_sample(q1, k1, q2, k2, *, P, K1, T1, T2, scale, lse_rest1=None,
+                       lse_rest2=None):
+    """Text sensitivity of every head for one image paired with two questions
+    (Sec. 3, Eq. (1)).  Each question is a stage-2 input of the layout of
+    inllm_sample (float64 q [S, H_q, d_h], k [S, H_kv, d_h]) with T1 / T2
+    valid text rows.  Returns the sensitivities, both profiles and both
+    questions' head variances u_h of Eq. (8)."""
+    out = {}
+    for c, (q, k, tb, rest) in enumerate(((q1, k1, T1, lse_rest1), (q2, k2, T2, lse_rest2))):
+        x = t2v_logits(q[P + K1:P + K1 + tb], k[P:P + K1], scale)
+        A, _ = t2v_attention(x, rest)
+        out[f"profile{c}"] = visual_profile(A)
+        out[f"head_var{c}"] = head_variance(A)
+    out["ts"] = text_sensitivity(out["profile0"], out["profile1"])
+    return out
+
+
+def sensitivity(q1, k1, q2, k2, text_len1, text_len2, dtype, *, P, K1, scale,
+                lse_rest1=None, lse_rest2=None):
+    """Batch form of sensitivity_sample on storage-form inputs
+    ([B, S, H, d_h]); text_len* [B] or None (= T_max = S - P - K1)."""
+    B, S = q1.shape[:2]
+    T_max = S - P - K1
+    keys = ("ts", "profile0", "profile1", "head_var0", "head_var1")
+    res = {key: [] for key in keys}
+    for b in range(B):
+        t1 = T_max if text_len1 is None else int(text_len1[b])
+        t2 = T_max if text_len2 is None else int(text_len2[b])
+        if not (1 <= t1 <= T_max and 1 <= t2 <= T_max):
+            raise ValueError("text_len out of range")
+        r = sensitivity_sample(
+            to_f64(q1[b], dtype), to_f64(k1[b], dtype), to_f64(q2[b], dtype), to_f64(k2[b], dtype),
+            P=P, K1=K1, T1=t1, T2=t2, scale=scale,
+            lse_rest1=None if lse_rest1 is None else lse_rest1[b][:, :t1],
+            lse_rest2=None if lse_rest2 is None else lse_rest2[b][:, :t2])
+        for key in keys:
+            res[key].append(r[key])
+    return {key: np.stack(val) for key, val in res.items()}
+
+
+def average_ranks(x):
+    """1-based ranks of x in ascending order; tied values share the mean of
+    the ranks they span."""
+    x = np.asarray(x, dtype=np.float64)
+    n = x.size
+    order = np.argsort(x, kind="stable")
+    xs = x[order]
+    ranks = np.empty(n)
+    i = 0
+    while i < n:
+        j = i
+        while j + 1 < n and xs[j + 1] == xs[i]:
+            j += 1
+        ranks[order[i:j + 1]] = (i + j) / 2.0 + 1.0
+        i = j + 1
+    return ranks
+
+
+def spearman(x, y):
+    """Spearman rank correlation: the Pearson correlation of the average ranks
+    of x and of y; NaN when either rank vector is constant."""
+    rx, ry = average_ranks(x), average_ranks(y)
+    dx, dy = rx - rx.mean(), ry - ry.mean()
+    den = math.sqrt((dx * dx).sum() * (dy * dy).sum())
+    return float("nan") if den == 0.0 else float((dx * dy).sum() / den)
+
+
+def topk_saliency_spearman(sv, st, k):
+    """Sec. 3 analysis: the Spearman correlation between visual saliency and
+    textual relevance over the k tokens with the highest saliency (the same
+    stable top-K as the pruning).  Returns (rho, kept indices ascending)."""
+    sv = np.asarray(sv, dtype=np.float64)
+    st = np.asarray(st, dtype=np.float64)
+    idx = topk_ascending(sv, k)
+    return spearman(sv[idx], st[idx]), idx
 
 
 def keep_count(ratio, n):

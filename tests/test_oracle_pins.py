@@ -332,3 +332,119 @@ def test_budget_split_brute_force_small():
             if best is None or key < best[0]:
                 best = (key, list(S))
         assert oracle.budget_split_topk(sv, st, k, rho).tolist() == best[1]
+
+
+# ------------------------------------------------------- Sec. 3 diagnostics
+def test_visual_profile_rows_and_single_row():
+    """Under the visual-only softmax each attention row sums to 1, so a
+    head's profile (the mean over text rows) sums to 1; with one text row it
+    is that row's softmax (library softmax)."""
+    x = RNG.standard_normal((4, 7, 30)) * 2
+    A, _ = oracle.t2v_attention(x)
+    prof = oracle.visual_profile(A)
+    assert prof.shape == (4, 30)
+    np.testing.assert_allclose(prof.sum(axis=-1), 1.0, rtol=1e-13)
+    one, _ = oracle.t2v_attention(x[:, :1])
+    np.testing.assert_allclose(oracle.visual_profile(one), scipy.special.softmax(x[:, 0], axis=-1),
+                               rtol=1e-13)
+
+
+def test_text_sensitivity_library_and_closed_forms():
+    """Eq. (1) against scikit-learn's cosine similarity, plus closed forms:
+    identical profiles give 0, profiles on disjoint tokens give 1, uniform
+    against one-hot over K tokens gives 1 - 1/sqrt(K); scaling a profile
+    changes nothing and the measure is symmetric."""
+    s1 = RNG.random((6, 50))
+    s2 = RNG.random((6, 50))
+    want = 1.0 - np.diag(cosine_similarity(s1, s2))
+    np.testing.assert_allclose(oracle.text_sensitivity(s1, s2), want, rtol=1e-12)
+    np.testing.assert_allclose(oracle.text_sensitivity(s2, s1), want, rtol=1e-12)
+    np.testing.assert_allclose(oracle.text_sensitivity(3.0 * s1, 0.5 * s2), want, rtol=1e-12)
+    np.testing.assert_allclose(oracle.text_sensitivity(s1, s1), 0.0, atol=1e-15)
+    K = 64
+    uni = np.full((1, K), 1.0 / K)
+    hot = np.zeros((1, K))
+    hot[0, 5] = 1.0
+    assert oracle.text_sensitivity(uni, hot)[0] == pytest.approx(1 - 1 / math.sqrt(K), rel=1e-14)
+    a = np.zeros((1, K))
+    b = np.zeros((1, K))
+    a[0, :10] = RNG.random(10)
+    b[0, 10:] = RNG.random(K - 10)
+    assert oracle.text_sensitivity(a, b)[0] == 1.0
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (6, 2)])
+def test_sensitivity_sample_matches_torch(Hq, Hkv):
+    """Both questions' profiles, head variances and sensitivities against an
+    independent float64 PyTorch computation (GQA by repeat_interleave,
+    library softmax), with different text lengths per question."""
+    S, P, K1, dh = 40, 3, 20, 16
+    q1, q2 = RNG.standard_normal((2, S, Hq, dh))
+    k1, k2 = RNG.standard_normal((2, S, Hkv, dh))
+    T1, T2, scale = 9, 4, 0.3
+    r = oracle.sensitivity_sample(q1, k1, q2, k2, P=P, K1=K1, T1=T1, T2=T2, scale=scale)
+    prof = []
+    for q, k, tb in ((q1, k1, T1), (q2, k2, T2)):
+        qt = torch.from_numpy(q[P + K1:P + K1 + tb]).permute(1, 0, 2)
+        kv = torch.from_numpy(k[P:P + K1]).permute(1, 0, 2).repeat_interleave(Hq // Hkv, dim=0)
+        A = torch.softmax(scale * qt @ kv.transpose(1, 2), dim=-1)
+        prof.append(A.mean(dim=1).numpy())
+        c = len(prof) - 1
+        np.testing.assert_allclose(r[f"profile{c}"], prof[c], rtol=1e-12)
+        np.testing.assert_allclose(r[f"head_var{c}"], A.var(dim=-1, unbiased=False).mean(dim=1).numpy(),
+                                   rtol=1e-11)
+    want = 1.0 - np.diag(cosine_similarity(prof[0], prof[1]))
+    np.testing.assert_allclose(r["ts"], want, rtol=1e-10)
+    same = oracle.sensitivity_sample(q1, k1, q1, k1, P=P, K1=K1, T1=T1, T2=T1, scale=scale)
+    np.testing.assert_allclose(same["ts"], 0.0, atol=1e-14)
+
+
+def test_average_ranks_library_and_hand_example():
+    assert oracle.average_ranks([10.0, 20.0, 20.0, 5.0]).tolist() == [2.0, 3.5, 3.5, 1.0]
+    for _ in range(5):
+        x = RNG.integers(0, 7, size=40).astype(np.float64)
+        np.testing.assert_array_equal(oracle.average_ranks(x), scipy.stats.rankdata(x, method="average"))
+    x = np.array([0.0, -0.0, 1.0])
+    assert oracle.average_ranks(x).tolist() == [1.5, 1.5, 3.0]
+
+
+def test_spearman_library_closed_form_and_invariants():
+    """Against SciPy (with ties), the tie-free closed form
+    1 - 6 sum d^2 / (n (n^2 - 1)), invariance under increasing maps, the
+    perfectly (anti)monotone cases and the constant case."""
+    for n in (5, 33, 200):
+        x = RNG.integers(0, 9, size=n).astype(np.float64)
+        y = RNG.integers(0, 5, size=n).astype(np.float64)
+        assert oracle.spearman(x, y) == pytest.approx(scipy.stats.spearmanr(x, y)[0], rel=1e-12, abs=1e-15)
+        x = RNG.permutation(n).astype(np.float64)
+        y = RNG.permutation(n).astype(np.float64)
+        d = x - y
+        closed = 1 - 6 * (d * d).sum() / (n * (n * n - 1))
+        assert oracle.spearman(x, y) == pytest.approx(closed, rel=1e-12, abs=1e-15)
+        assert oracle.spearman(np.exp(x / n), y ** 3) == pytest.approx(closed, rel=1e-12, abs=1e-15)
+        assert oracle.spearman(x, 2 * x + 1) == pytest.approx(1.0, rel=1e-15)
+        assert oracle.spearman(x, -x) == pytest.approx(-1.0, rel=1e-15)
+    assert math.isnan(oracle.spearman(np.ones(5), np.arange(5.0)))
+    assert math.isnan(oracle.spearman([1.0], [2.0]))
+
+
+def test_topk_saliency_spearman_brute_force():
+    """The set is the top-K of s^v in the pruning's stable order, found here
+    by sorting (-s^v, index) tuples; K = N correlates the whole vectors."""
+    for seed in range(6):
+        rng = np.random.default_rng(seed)
+        N = 25
+        sv = rng.integers(0, 6, size=N).astype(np.float64)
+        st = rng.standard_normal(N)
+        st[rng.random(N) < 0.3] = 0.0
+        K = int(rng.integers(2, N))
+        idx = sorted(sorted(range(N), key=lambda i: (-sv[i], i))[:K])
+        rho, got = oracle.topk_saliency_spearman(sv, st, K)
+        assert got.tolist() == idx
+        want = scipy.stats.spearmanr(sv[idx], st[idx])[0]
+        if math.isnan(want):
+            assert math.isnan(rho)
+        else:
+            assert rho == pytest.approx(want, rel=1e-12, abs=1e-15)
+        full, _ = oracle.topk_saliency_spearman(sv, st, N)
+        assert full == pytest.approx(scipy.stats.spearmanr(sv, st)[0], rel=1e-12, abs=1e-15)
