@@ -174,6 +174,58 @@ typedef struct trevs_inllm_args {
   void* const* events;       /* OPTIONAL [2*TREVS_INLLM_NUM_KERNELS] hipEvent_t */
 } trevs_inllm_args;
 
+/* ------------------------------------------------------------------------
+ * Diagnostics of the preliminary analysis (Sec. 3), computed on the same
+ * tensors as the pruning stages.
+ *
+ * Text sensitivity of the attention heads (Eq. (1)).  One image paired with
+ * two questions gives two stage-2 inputs of one shape, each laid out as for
+ * trevs_inllm_prune (visual rows [P,P+K_in), text rows after them).  For
+ * question c in {0,1} with T^c_b = text_len[c][b] valid text rows:
+ *   A^c[h,q,:]  = the text->vision attention of trevs_inllm_prune (visual-only
+ *                 softmax, or the full row when lse_rest[c] is given)
+ *   s^c_h       = (1/T^c_b) sum_{q<T^c_b} A^c[h,q,:]   the head's attention
+ *                 distribution over the visual tokens for that question
+ *   ts[b,h]     = 1 - cos(s^0_h, s^1_h)                                 Eq. (1)
+ * head_var[c] optionally receives u_h of Eq. (8) for question c, so that the
+ * heads can be ranked by attention variance as in the analysis.
+ * ---------------------------------------------------------------------- */
+typedef struct trevs_sensitivity_args {
+  uint32_t struct_size;      /* sizeof(trevs_sensitivity_args) */
+  int32_t B, S, P, K_in, T_max;  /* as in trevs_inllm_args; P + K_in + T_max <= S */
+  int32_t H_q, H_kv;         /* query / key-value heads; H_q % H_kv == 0 */
+  int32_t d_head;            /* 64, 128 or 256 */
+  float scale;               /* logit scale > 0 */
+  int32_t dtype;             /* trevs_dtype of q and k */
+  const void* q[2];          /* per question [B,S,H_q,d_head] (16-byte aligned) */
+  const void* k[2];          /* per question [B,S,H_kv,d_head] (16-byte aligned); may be one buffer */
+  const int32_t* text_len[2];  /* per question [B] in 1..T_max, or NULL (= T_max) */
+  const float* lse_rest[2];  /* OPTIONAL per question [B,H_q,T_max] non-visual log-sum-exp */
+  float* ts;                 /* OUT [B,H_q] text sensitivity */
+  float* profile[2];         /* OPTIONAL OUT per question [B,H_q,K_in] s^c_h */
+  float* head_var[2];        /* OPTIONAL OUT per question [B,H_q] u_h */
+} trevs_sensitivity_args;
+
+size_t trevs_sensitivity_workspace_size(const trevs_sensitivity_args* args);
+trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* args, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
+/* Spearman rank correlation between visual saliency and textual relevance
+ * within the top-K saliency set (Sec. 3).  sv, st [B,N] are s^v and s^t
+ * (device, finite fp32; e.g. sal_out and rel_out of trevs_prellm_prune).
+ * Per sample b: the K tokens first under (sv desc, index asc), the same
+ * stable top-K as the pruning; the 1-based ranks of sv and of st over those
+ * K tokens, tied values sharing the mean of the ranks they span; rho[b] =
+ * the Pearson correlation of the two rank vectors, NaN when either is
+ * constant (always for K = 1).  The rank sums are exact integers, so rho is
+ * correctly rounded up to one division and one square root in double.
+ * kept_idx: OPTIONAL OUT [B,K] the set, ascending.  N in
+ * 1..TREVS_MAX_SELECT_N, K in 1..N. */
+size_t trevs_spearman_workspace_size(int32_t B, int32_t N, int32_t K);
+trevs_status trevs_topk_spearman(const float* sv, const float* st, int32_t B, int32_t N, int32_t K,
+                                 double* rho, int32_t* kept_idx, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
 /* Workspace bytes the call needs for these arguments (0 on invalid args).
  * The workspace must be 256-byte aligned; its contents need no initialisation
  * and are garbage afterwards. */
@@ -206,6 +258,7 @@ int32_t trevs_keep_count(float ratio, int32_t n);
  * bindings that mirror them. */
 size_t trevs_prellm_args_size(void);
 size_t trevs_inllm_args_size(void);
+size_t trevs_sensitivity_args_size(void);
 
 #ifdef __cplusplus
 }

@@ -192,23 +192,37 @@ trevs_status validate_inllm(const trevs_inllm_args* a) {
 // Split of the visual keys for the statistics pass: enough workgroups to fill
 // the GPU (>= 2 per CU), each split at least 256 keys, lengths multiples of 64
 // (the pass consumes key tiles in pairs of 32).
+struct StatsPlan {
+  int n_split, split_len, n_rgroups;
+};
+StatsPlan stats_plan(int B, int K_in, int T_max, int H_q, int H_kv) {
+  StatsPlan p;
+  const int G = H_q / H_kv;
+  const int nrb = (G * T_max + 31) / 32;
+  const int nw = stats_waves(G, T_max);
+  p.n_rgroups = (nrb + nw - 1) / nw;
+  const int64_t base_wgs = (int64_t)B * H_kv * p.n_rgroups;
+  int n_split = (int)std::min<int64_t>((512 + base_wgs - 1) / base_wgs, (K_in + 255) / 256);
+  n_split = std::max(n_split, 1);
+  p.split_len = ((K_in + n_split - 1) / n_split + 63) / 64 * 64;
+  p.n_split = (K_in + p.split_len - 1) / p.split_len;
+  return p;
+}
+
+size_t lse_rows_padded(int T_max) { return (size_t)(T_max + 31) / 32 * 32; }
+
 InllmPlan inllm_plan(const trevs_inllm_args* a) {
   InllmPlan p;
-  const int G = a->H_q / a->H_kv;
-  const int nrb = (G * a->T_max + 31) / 32;
-  const int nw = stats_waves(G, a->T_max);
-  p.n_rgroups = (nrb + nw - 1) / nw;
-  const int64_t base_wgs = (int64_t)a->B * a->H_kv * p.n_rgroups;
-  int n_split = (int)std::min<int64_t>((512 + base_wgs - 1) / base_wgs, (a->K_in + 255) / 256);
-  n_split = std::max(n_split, 1);
-  p.split_len = ((a->K_in + n_split - 1) / n_split + 63) / 64 * 64;
-  p.n_split = (a->K_in + p.split_len - 1) / p.split_len;
+  const StatsPlan sp = stats_plan(a->B, a->K_in, a->T_max, a->H_q, a->H_kv);
+  p.n_split = sp.n_split;
+  p.split_len = sp.split_len;
+  p.n_rgroups = sp.n_rgroups;
   const size_t rows = (size_t)a->B * a->H_q * a->T_max;
   size_t off = 0;
   p.part = off;
   off = align_up(off + rows * p.n_split * sizeof(float4));
   p.lse2 = off;
-  off = align_up(off + (size_t)a->B * a->H_q * ((a->T_max + 31) / 32 * 32) * sizeof(float));
+  off = align_up(off + (size_t)a->B * a->H_q * lse_rows_padded(a->T_max) * sizeof(float));
   p.head_var = off;
   off = align_up(off + (size_t)a->B * a->H_q * sizeof(float));
   p.head_sel = off;
@@ -218,6 +232,80 @@ InllmPlan inllm_plan(const trevs_inllm_args* a) {
   p.total = off;
   return p;
 }
+
+// ------------------------------------------------------------------ analysis
+trevs_status validate_sensitivity(const trevs_sensitivity_args* a) {
+  if (!a || a->struct_size != sizeof(trevs_sensitivity_args)) return TREVS_ERR_INVALID_ARG;
+  if (a->dtype != TREVS_F32 && a->dtype != TREVS_BF16) return TREVS_ERR_INVALID_ARG;
+  if (a->B < 1 || a->S < 1 || a->P < 0 || a->K_in < 1 || a->T_max < 1) return TREVS_ERR_INVALID_ARG;
+  if ((int64_t)a->P + a->K_in + a->T_max > a->S) return TREVS_ERR_INVALID_ARG;
+  if (a->H_q < 1 || a->H_kv < 1 || a->H_q % a->H_kv || a->d_head < 1) return TREVS_ERR_INVALID_ARG;
+  if (!finite(a->scale) || a->scale <= 0.f) return TREVS_ERR_INVALID_ARG;
+  if (!a->ts || !aligned(a->ts, 4)) return TREVS_ERR_INVALID_ARG;
+  const int e = elem_bytes(a->dtype);
+  const size_t B = a->B, S = a->S;
+  Span in[8], out[5];
+  out[0] = Span{a->ts, B * a->H_q * 4};
+  for (int c = 0; c < 2; ++c) {
+    if (!a->q[c] || !a->k[c] || !aligned(a->q[c], 16) || !aligned(a->k[c], 16) ||
+        !aligned(a->text_len[c], 4) || !aligned(a->lse_rest[c], 4) || !aligned(a->profile[c], 4) ||
+        !aligned(a->head_var[c], 4))
+      return TREVS_ERR_INVALID_ARG;
+    in[4 * c + 0] = Span{a->q[c], B * S * a->H_q * a->d_head * e};
+    in[4 * c + 1] = Span{a->k[c], B * S * a->H_kv * a->d_head * e};
+    in[4 * c + 2] = Span{a->text_len[c], a->text_len[c] ? B * 4 : 0};
+    in[4 * c + 3] = Span{a->lse_rest[c], a->lse_rest[c] ? B * a->H_q * a->T_max * 4 : 0};
+    out[1 + 2 * c] = Span{a->profile[c], a->profile[c] ? B * a->H_q * a->K_in * 4 : 0};
+    out[2 + 2 * c] = Span{a->head_var[c], a->head_var[c] ? B * a->H_q * 4 : 0};
+  }
+  if (any_overlap(out, 5, in, 8)) return TREVS_ERR_INVALID_ARG;
+  if ((int64_t)a->B * a->S > INT32_MAX || (int64_t)a->B * a->H_q * a->T_max > INT32_MAX ||
+      (int64_t)a->B * a->H_q * a->K_in > INT32_MAX)
+    return TREVS_ERR_UNSUPPORTED;
+  if (a->d_head != 64 && a->d_head != 128 && a->d_head != 256) return TREVS_ERR_UNSUPPORTED;
+  return TREVS_OK;
+}
+
+struct SensitivityLayout {
+  StatsPlan sp;
+  size_t part[2], lse2[2], head_var[2], profile[2], total;
+};
+
+SensitivityLayout sensitivity_layout(const trevs_sensitivity_args* a) {
+  SensitivityLayout L;
+  L.sp = stats_plan(a->B, a->K_in, a->T_max, a->H_q, a->H_kv);
+  const size_t heads = (size_t)a->B * a->H_q;
+  size_t off = 0;
+  for (int c = 0; c < 2; ++c) {
+    L.part[c] = off;
+    off = align_up(off + heads * a->T_max * L.sp.n_split * sizeof(float4));
+    L.lse2[c] = off;
+    off = align_up(off + heads * lse_rows_padded(a->T_max) * sizeof(float));
+    L.head_var[c] = off;
+    off = align_up(off + heads * sizeof(float));
+    L.profile[c] = off;
+    off = align_up(off + heads * a->K_in * sizeof(float));
+  }
+  L.total = off;
+  return L;
+}
+
+size_t spearman_tiles(int K) { return (size_t)(K + kRankTile - 1) / kRankTile; }
+
+trevs_status validate_spearman(const float* sv, const float* st, int32_t B, int32_t N, int32_t K,
+                               const double* rho, const int32_t* kept_idx) {
+  if (!sv || !st || !rho || B < 1 || N < 1 || K < 1 || K > N) return TREVS_ERR_INVALID_ARG;
+  if (!aligned(sv, 4) || !aligned(st, 4) || !aligned(rho, 8) || !aligned(kept_idx, 4))
+    return TREVS_ERR_INVALID_ARG;
+  const Span in[] = {{sv, (size_t)B * N * 4}, {st, (size_t)B * N * 4}};
+  const Span out[] = {{rho, (size_t)B * 8}, {kept_idx, kept_idx ? (size_t)B * K * 4 : 0}};
+  if (any_overlap(out, 2, in, 2)) return TREVS_ERR_INVALID_ARG;
+  if ((int64_t)B * N > INT32_MAX) return TREVS_ERR_UNSUPPORTED;
+  if (N > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
+  return TREVS_OK;
+}
+
+size_t spearman_ws_part(int32_t B, int32_t K) { return align_up((size_t)B * K * sizeof(int32_t)); }
 
 trevs_status check_ws(void* ws, size_t ws_bytes, size_t need) {
   if (need == 0) return TREVS_OK;
@@ -241,6 +329,7 @@ extern "C" {
 
 size_t trevs_prellm_args_size(void) { return sizeof(trevs_prellm_args); }
 size_t trevs_inllm_args_size(void) { return sizeof(trevs_inllm_args); }
+size_t trevs_sensitivity_args_size(void) { return sizeof(trevs_sensitivity_args); }
 
 const char* trevs_status_string(trevs_status s) {
   switch (s) {
@@ -446,7 +535,7 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   ha.B = a->B;
   ha.H_q = a->H_q;
   ha.T_max = a->T_max;
-  ha.T_pad = (a->T_max + 31) / 32 * 32;
+  ha.T_pad = (int)lse_rows_padded(a->T_max);
   ha.K_in = a->K_in;
   ha.n_split = p.n_split;
   ha.text_len = a->text_len;
@@ -465,7 +554,7 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   sa.P = a->P;
   sa.K_in = a->K_in;
   sa.T_max = a->T_max;
-  sa.T_pad = (a->T_max + 31) / 32 * 32;
+  sa.T_pad = (int)lse_rows_padded(a->T_max);
   sa.H_q = a->H_q;
   sa.H_kv = a->H_kv;
   sa.G = G;
@@ -526,6 +615,109 @@ trevs_status trevs_topk_select(const float* scores, int32_t B, int32_t N, int32_
     return TREVS_ERR_INVALID_ARG;
   if (N > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
   TREVS_HIP(launch_topk(scores, B, N, K, kept_idx, reinterpret_cast<hipStream_t>(stream)));
+  return TREVS_OK;
+}
+
+size_t trevs_sensitivity_workspace_size(const trevs_sensitivity_args* a) {
+  if (validate_sensitivity(a) != TREVS_OK) return 0;
+  return sensitivity_layout(a).total;
+}
+
+trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* a, void* ws, size_t ws_bytes, void* stream) {
+  TREVS_TRY(validate_sensitivity(a));
+  const SensitivityLayout L = sensitivity_layout(a);
+  TREVS_TRY(check_ws(ws, ws_bytes, L.total));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = reinterpret_cast<uint8_t*>(ws);
+  const int G = a->H_q / a->H_kv;
+  const int T_pad = (int)lse_rows_padded(a->T_max);
+  const int tile = score_tile_tokens(a->dtype, a->d_head);
+  SensitivityArgs sa;
+  sa.H_q = a->H_q;
+  sa.K_in = a->K_in;
+  sa.ts = a->ts;
+  for (int c = 0; c < 2; ++c) {
+    float4* part = reinterpret_cast<float4*>(w + L.part[c]);
+    float* lse2 = reinterpret_cast<float*>(w + L.lse2[c]);
+    float* head_var = a->head_var[c] ? a->head_var[c] : reinterpret_cast<float*>(w + L.head_var[c]);
+    float* profile = a->profile[c] ? a->profile[c] : reinterpret_cast<float*>(w + L.profile[c]);
+    StatsArgs ta;
+    ta.q = a->q[c];
+    ta.k = a->k[c];
+    ta.B = a->B;
+    ta.S = a->S;
+    ta.P = a->P;
+    ta.K_in = a->K_in;
+    ta.T_max = a->T_max;
+    ta.H_q = a->H_q;
+    ta.H_kv = a->H_kv;
+    ta.G = G;
+    ta.scale_log2e = a->scale * kLog2e;
+    ta.n_split = L.sp.n_split;
+    ta.split_len = L.sp.split_len;
+    ta.n_rgroups = L.sp.n_rgroups;
+    ta.part = part;
+    TREVS_HIP(launch_stats(ta, a->dtype, a->d_head, s));
+    HeadArgs ha;
+    ha.part = part;
+    ha.B = a->B;
+    ha.H_q = a->H_q;
+    ha.T_max = a->T_max;
+    ha.T_pad = T_pad;
+    ha.K_in = a->K_in;
+    ha.n_split = L.sp.n_split;
+    ha.text_len = a->text_len[c];
+    ha.lse_rest = a->lse_rest[c];
+    ha.lse2 = lse2;
+    ha.head_var = head_var;
+    TREVS_HIP(launch_heads(ha, s));
+    ProfileArgs pa;
+    pa.q = a->q[c];
+    pa.k = a->k[c];
+    pa.B = a->B;
+    pa.S = a->S;
+    pa.P = a->P;
+    pa.K_in = a->K_in;
+    pa.T_max = a->T_max;
+    pa.T_pad = T_pad;
+    pa.H_q = a->H_q;
+    pa.H_kv = a->H_kv;
+    pa.G = G;
+    pa.n_vtiles = (a->K_in + tile - 1) / tile;
+    pa.scale_log2e = a->scale * kLog2e;
+    pa.lse2 = lse2;
+    pa.text_len = a->text_len[c];
+    pa.profile = profile;
+    TREVS_HIP(launch_profile(pa, a->dtype, a->d_head, s));
+    sa.profile[c] = profile;
+  }
+  TREVS_HIP(launch_sensitivity(sa, a->B, s));
+  return TREVS_OK;
+}
+
+size_t trevs_spearman_workspace_size(int32_t B, int32_t N, int32_t K) {
+  if (B < 1 || N < 1 || K < 1 || K > N || N > TREVS_MAX_SELECT_N || (int64_t)B * N > INT32_MAX) return 0;
+  return spearman_ws_part(B, K) + align_up((size_t)B * spearman_tiles(K) * 4 * sizeof(long long));
+}
+
+trevs_status trevs_topk_spearman(const float* sv, const float* st, int32_t B, int32_t N, int32_t K, double* rho,
+                                 int32_t* kept_idx, void* ws, size_t ws_bytes, void* stream) {
+  TREVS_TRY(validate_spearman(sv, st, B, N, K, rho, kept_idx));
+  TREVS_TRY(check_ws(ws, ws_bytes, trevs_spearman_workspace_size(B, N, K)));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = reinterpret_cast<uint8_t*>(ws);
+  int32_t* idx = kept_idx ? kept_idx : reinterpret_cast<int32_t*>(w);
+  TREVS_HIP(launch_topk(sv, B, N, K, idx, s));
+  SpearmanArgs pa;
+  pa.sv = sv;
+  pa.st = st;
+  pa.idx = idx;
+  pa.N = N;
+  pa.K = K;
+  pa.n_tiles = (int)spearman_tiles(K);
+  pa.part = reinterpret_cast<long long*>(w + spearman_ws_part(B, K));
+  pa.rho = rho;
+  TREVS_HIP(launch_spearman(pa, B, s));
   return TREVS_OK;
 }
 

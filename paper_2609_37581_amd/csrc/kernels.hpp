@@ -102,6 +102,37 @@ struct FpsArgs {
 // Gram matrix, initial distances and the K_d sequential picks.
 hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hipStream_t s);
 
+// ---------------------------------------------------------------- analysis
+struct ProfileArgs {
+  const void* q;
+  const void* k;
+  int B, S, P, K_in, T_max, T_pad, H_q, H_kv, G;
+  int n_vtiles;              // workgroups per (sample, head)
+  float scale_log2e;
+  const float* lse2;         // [B,H_q,T_pad] row log-sum-exp in log2 units
+  const int32_t* text_len;
+  float* profile;            // [B,H_q,K_in] mean attention over the valid text rows
+};
+struct SensitivityArgs {
+  const float* profile[2];   // [B,H_q,K_in] per question
+  int H_q, K_in;
+  float* ts;                 // [B,H_q]
+};
+struct SpearmanArgs {
+  const float* sv;           // [B,N]
+  const float* st;           // [B,N]
+  const int32_t* idx;        // [B,K] the top-K saliency set
+  int N, K, n_tiles;         // n_tiles = ceil(K / kRankTile)
+  long long* part;           // [B,n_tiles,4] partial sums of the centred rank products
+  double* rho;               // [B]
+};
+constexpr int kRankTile = 64;  // tokens ranked per workgroup (one per lane)
+// Visual profiles of every head for one question, the sensitivity of each
+// head between two questions, and the rank correlation within a top-K set.
+hipError_t launch_profile(const ProfileArgs& a, int dtype, int dh, hipStream_t s);
+hipError_t launch_sensitivity(const SensitivityArgs& a, int B, hipStream_t s);
+hipError_t launch_spearman(const SpearmanArgs& a, int B, hipStream_t s);
+
 // ---------------------------------------------------------------- gather
 constexpr int kGatherMaxTensors = 4;
 struct GatherTensor {

@@ -62,6 +62,15 @@ class InllmArgs(ctypes.Structure):
                 ("events", c_void_p)]
 
 
+class SensitivityArgs(ctypes.Structure):
+    _fields_ = [("struct_size", c_uint32), ("B", c_int32), ("S", c_int32), ("P", c_int32),
+                ("K_in", c_int32), ("T_max", c_int32), ("H_q", c_int32), ("H_kv", c_int32),
+                ("d_head", c_int32), ("scale", c_float), ("dtype", c_int32),
+                ("q", c_void_p * 2), ("k", c_void_p * 2), ("text_len", c_void_p * 2),
+                ("lse_rest", c_void_p * 2), ("ts", c_void_p), ("profile", c_void_p * 2),
+                ("head_var", c_void_p * 2)]
+
+
 _lib = None
 
 
@@ -90,10 +99,22 @@ def lib():
         L.trevs_status_string.restype = ctypes.c_char_p
         L.trevs_keep_count.argtypes = [c_float, c_int32]
         L.trevs_keep_count.restype = c_int32
+        L.trevs_sensitivity_workspace_size.argtypes = [ctypes.POINTER(SensitivityArgs)]
+        L.trevs_sensitivity_workspace_size.restype = c_size_t
+        L.trevs_text_sensitivity.argtypes = [ctypes.POINTER(SensitivityArgs), c_void_p, c_size_t,
+                                             c_void_p]
+        L.trevs_text_sensitivity.restype = ctypes.c_int
+        L.trevs_spearman_workspace_size.argtypes = [c_int32, c_int32, c_int32]
+        L.trevs_spearman_workspace_size.restype = c_size_t
+        L.trevs_topk_spearman.argtypes = [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p,
+                                          c_void_p, c_void_p, c_size_t, c_void_p]
+        L.trevs_topk_spearman.restype = ctypes.c_int
         L.trevs_prellm_args_size.restype = c_size_t
         L.trevs_inllm_args_size.restype = c_size_t
+        L.trevs_sensitivity_args_size.restype = c_size_t
         if (L.trevs_prellm_args_size() != ctypes.sizeof(PrellmArgs)
-                or L.trevs_inllm_args_size() != ctypes.sizeof(InllmArgs)):
+                or L.trevs_inllm_args_size() != ctypes.sizeof(InllmArgs)
+                or L.trevs_sensitivity_args_size() != ctypes.sizeof(SensitivityArgs)):
             raise RuntimeError("libtrevs.so argument structs do not match this binding")
         _lib = L
     return _lib
@@ -315,6 +336,92 @@ def topk_select(scores, k, stream=None):
     if st:
         raise TrevsError(st, "trevs_topk_select")
     return out
+
+
+# ---------------------------------------------------------------- diagnostics
+class TextSensitivity:
+    """Eq. (1) for every head (Sec. 3): one image with two questions, each a
+    stage-2 input (q [B,S,H_q,d_h], k [B,S,H_kv,d_h], same shapes).  Outputs
+    ts [B,H_q] and, per question, the visual profiles [B,H_q,K_in] and head
+    variances [B,H_q]; allocated once, call() enqueues the computation."""
+
+    def __init__(self, q, k, q2, k2, text_len=None, text_len2=None, *, P, K_in, scale=None,
+                 lse_rest=None, lse_rest2=None):
+        dev = q.device
+        dt = q.dtype
+        for t, name in ((q, "q"), (k, "k"), (q2, "q2"), (k2, "k2")):
+            _check(t, name, dev, 4, dt)
+        for t, name in ((text_len, "text_len"), (text_len2, "text_len2")):
+            if t is not None:
+                _check(t, name, dev, 1, torch.int32)
+        B, S, H_q, d_head = q.shape
+        H_kv = k.shape[2]
+        T_max = S - P - K_in
+        if q2.shape != q.shape or k.shape != (B, S, H_kv, d_head) or k2.shape != k.shape:
+            raise ValueError("inconsistent shapes of the two questions")
+        if T_max < 1:
+            raise ValueError("no text rows after the visual block")
+        for t, name in ((lse_rest, "lse_rest"), (lse_rest2, "lse_rest2")):
+            if t is not None:
+                _check(t, name, dev, 3, torch.float32)
+                if t.shape != (B, H_q, T_max):
+                    raise ValueError(f"{name} must be [B,H_q,T_max]")
+        self.inputs = (q, k, q2, k2, text_len, text_len2, lse_rest, lse_rest2)
+        self.ts = torch.empty((B, H_q), dtype=torch.float32, device=dev)
+        self.profile = [torch.empty((B, H_q, K_in), dtype=torch.float32, device=dev) for _ in range(2)]
+        self.head_var = [torch.empty((B, H_q), dtype=torch.float32, device=dev) for _ in range(2)]
+        a = SensitivityArgs()
+        a.struct_size = ctypes.sizeof(SensitivityArgs)
+        a.B, a.S, a.P, a.K_in, a.T_max = B, S, P, K_in, T_max
+        a.H_q, a.H_kv, a.d_head = H_q, H_kv, d_head
+        a.scale = float(scale) if scale is not None else d_head ** -0.5
+        a.dtype = _dtype_code(q)
+        a.q[0], a.q[1], a.k[0], a.k[1] = _ptr(q), _ptr(q2), _ptr(k), _ptr(k2)
+        a.text_len[0], a.text_len[1] = _ptr(text_len), _ptr(text_len2)
+        a.lse_rest[0], a.lse_rest[1] = _ptr(lse_rest), _ptr(lse_rest2)
+        a.ts = _ptr(self.ts)
+        a.profile[0], a.profile[1] = _ptr(self.profile[0]), _ptr(self.profile[1])
+        a.head_var[0], a.head_var[1] = _ptr(self.head_var[0]), _ptr(self.head_var[1])
+        self.args = a
+        ws = lib().trevs_sensitivity_workspace_size(ctypes.byref(a))
+        if ws == 0:
+            st = lib().trevs_text_sensitivity(ctypes.byref(a), None, 0, None)
+            raise TrevsError(st, "trevs_text_sensitivity")
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
+
+    def __call__(self, stream=None):
+        st = lib().trevs_text_sensitivity(ctypes.byref(self.args), self.workspace.data_ptr(),
+                                          self.workspace.numel(), _stream(stream))
+        if st:
+            raise TrevsError(st, "trevs_text_sensitivity")
+        return self.ts
+
+
+def text_sensitivity(q, k, q2, k2, text_len=None, text_len2=None, **kw):
+    """Eq. (1): returns (ts [B,H_q], [profile0, profile1], [head_var0, head_var1])."""
+    call = TextSensitivity(q, k, q2, k2, text_len, text_len2, **kw)
+    call()
+    return call.ts, call.profile, call.head_var
+
+
+def topk_spearman(sv, st, k, stream=None):
+    """Spearman correlation of s^v and s^t within the top-k saliency set of
+    each sample (Sec. 3).  sv, st [B,N] fp32 on the device.  Returns
+    (rho float64 [B], kept_idx int32 [B,k] ascending)."""
+    _check(sv, "sv", sv.device, 2, torch.float32)
+    _check(st, "st", sv.device, 2, torch.float32)
+    if st.shape != sv.shape:
+        raise ValueError("sv and st must have one shape")
+    B, N = sv.shape
+    rho = torch.empty(B, dtype=torch.float64, device=sv.device)
+    idx = torch.empty((B, k), dtype=torch.int32, device=sv.device)
+    ws_bytes = lib().trevs_spearman_workspace_size(B, N, k)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=sv.device)
+    stat = lib().trevs_topk_spearman(sv.data_ptr(), st.data_ptr(), B, N, k, rho.data_ptr(),
+                                     idx.data_ptr(), ws.data_ptr(), ws_bytes, _stream(stream))
+    if stat:
+        raise TrevsError(stat, "trevs_topk_spearman")
+    return rho, idx
 
 
 # ---------------------------------------------------------------- HIP events

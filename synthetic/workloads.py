@@ -286,3 +286,57 @@ def stage2_inputs(w, with_lse_rest=False):
         sens_sets.append(sens)
     return dict(q=q, k=k, v=v, hidden=hidden, pos=pos, text_len=lens,
                 lse_rest=lse_rest, relevant=rel_sets, sensitive=sens_sets)
+
+
+def sensitivity_inputs(w, rephrase=0.1, with_lse_rest=False):
+    """Two questions about one image for the text-sensitivity analysis.
+
+    Layout per question as in stage2_inputs.  The image's key rows are shared
+    by both questions (k [B,S,H_kv,d_h]); two unit directions per KV group are
+    planted in two disjoint sets of visual key rows.  Question 0's query rows
+    are N(0,1) scaled per head by a permutation of linspace(0.5, 2, H_q);
+    question 1 repeats them plus `rephrase` * N(0,1) (a reworded question),
+    except that on a quarter of the heads ("sensitive") the text rows carry
+    the first direction in question 0 and the second in question 1.  Text
+    lengths are drawn per question.  Returns dict: q0, q1, k, text_len0,
+    text_len1, optionally lse_rest0/lse_rest1 [B,H_q,T_max], sensitive."""
+    B, S, Hq, Hkv, dh = w.B, w.S, w.H_q, w.H_kv, w.d_h
+    G = Hq // Hkv
+    sd = np.float32 if w.dtype == "f32" else np.uint16
+    q0 = np.empty((B, S, Hq, dh), dtype=sd)
+    q1 = np.empty((B, S, Hq, dh), dtype=sd)
+    k = np.empty((B, S, Hkv, dh), dtype=sd)
+    lens0 = _text_lengths(w)
+    lens1 = _text_lengths(w.with_(seed=w.seed + 17))
+    lse = [np.empty((B, Hq, w.T_max), dtype=np.float32) for _ in range(2)] if with_lse_rest else None
+    sens_sets = []
+    a = math.sqrt(3.0 * math.sqrt(dh))
+    T0 = w.P + w.K1
+    for b in range(B):
+        rng = _rng(w, 3, b)
+        beta = rng.permutation(np.linspace(0.5, 2.0, Hq)).astype(np.float32)
+        Q = rng.standard_normal((S, Hq, dh), dtype=np.float32) * beta[None, :, None]
+        Q1 = Q + np.float32(rephrase) * rng.standard_normal((S, Hq, dh), dtype=np.float32)
+        Kt = rng.standard_normal((S, Hkv, dh), dtype=np.float32)
+        sens = np.sort(rng.choice(Hq, size=max(1, Hq // 4), replace=False))
+        n_rel = min(max(1, w.K1 // 8), w.K1 // 2)  # none when there is a single visual row
+        rows = rng.choice(w.K1, size=2 * n_rel, replace=False)
+        c = rng.standard_normal((2, Hkv, dh))
+        c /= np.linalg.norm(c, axis=2, keepdims=True)
+        for g in range(Hkv):
+            Kt[w.P + rows[:n_rel], g, :] += (a * c[0, g]).astype(np.float32)
+            Kt[w.P + rows[n_rel:], g, :] += (a * c[1, g]).astype(np.float32)
+        for h in sens:
+            Q[T0:, h, :] += (a * c[0, h // G]).astype(np.float32)
+            Q1[T0:, h, :] = Q[T0:, h, :] - (a * c[0, h // G]).astype(np.float32) + (a * c[1, h // G]).astype(np.float32)
+        q0[b] = to_storage(Q, w.dtype)
+        q1[b] = to_storage(Q1, w.dtype)
+        k[b] = to_storage(Kt, w.dtype)
+        if with_lse_rest:
+            for c_ in range(2):
+                lse[c_][b] = (rng.standard_normal((Hq, w.T_max))
+                              + np.log(w.P + 1 + np.arange(w.T_max))[None, :])
+        sens_sets.append(sens)
+    return dict(q0=q0, q1=q1, k=k, text_len0=lens0, text_len1=lens1,
+                lse_rest0=None if lse is None else lse[0], lse_rest1=None if lse is None else lse[1],
+                sensitive=sens_sets)

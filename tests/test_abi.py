@@ -42,6 +42,7 @@ def test_struct_mirror_sizes():
     L = trevs.lib()
     assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 168
     assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 192
+    assert L.trevs_sensitivity_args_size() == ctypes.sizeof(trevs.SensitivityArgs) == 152
 
 
 def test_status_strings_and_keep_count():
@@ -139,3 +140,61 @@ def test_topk_rejects_before_launch():
     assert L.trevs_topk_select(None, 1, 10, 1, (1 << 40) + (1 << 32), None, 0, None) == 1
     assert L.trevs_topk_select(1 << 40, 1, 40000, 1, (1 << 40) + (1 << 32), None, 0, None) == 2
     assert L.trevs_topk_select(1 << 40, 1, 10, 5, (1 << 40) + 8, None, 0, None) == 1  # overlap
+
+
+def _sens(**kw):
+    a = trevs.SensitivityArgs()
+    a.struct_size = ctypes.sizeof(a)
+    a.B, a.S, a.P, a.K_in, a.T_max = 2, 259, 35, 192, 32
+    a.H_q, a.H_kv, a.d_head, a.scale, a.dtype = 32, 32, 128, 128 ** -0.5, trevs.TREVS_BF16
+    base = 1 << 40
+    a.q[0], a.q[1] = base, base + (1 << 32)
+    a.k[0] = a.k[1] = base + (2 << 32)  # one image: both questions may share the keys
+    a.ts = base + (3 << 32)
+    for k, v in kw.items():
+        if isinstance(v, tuple):
+            getattr(a, k)[v[0]] = v[1]
+        else:
+            setattr(a, k, v)
+    return a
+
+
+def test_sensitivity_workspace_covers_both_questions():
+    L = trevs.lib()
+    a = _sens()
+    ws = L.trevs_sensitivity_workspace_size(ctypes.byref(a))
+    # both questions' profiles [B,H_q,K_in] live in the workspace when not requested
+    assert ws >= 2 * 2 * 32 * 192 * 4
+    assert L.trevs_text_sensitivity(ctypes.byref(a), None, 0, None) == 3
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(T_max=300), 1), (dict(H_kv=5), 1), (dict(scale=float("inf")), 1), (dict(P=-1), 1),
+    (dict(ts=None), 1), (dict(q=(1, None)), 1), (dict(k=(0, (1 << 40) + 8)), 1),
+    (dict(d_head=96), 2), (dict(struct_size=8), 1), (dict(dtype=3), 1),
+    (dict(ts=(1 << 40) + (2 << 32) + 64), 1),  # overlaps the keys
+    (dict(profile=(1, (1 << 40) + 1024)), 1),  # overlaps question 0's queries
+    (dict(head_var=(0, (1 << 40) + (5 << 32) + 2)), 1),  # misaligned
+])
+def test_sensitivity_rejects_before_launch(bad, code):
+    L = trevs.lib()
+    a = _sens(**bad)
+    assert L.trevs_sensitivity_workspace_size(ctypes.byref(a)) == 0
+    assert L.trevs_text_sensitivity(ctypes.byref(a), None, 0, None) == code
+
+
+def test_spearman_rejects_before_launch():
+    L = trevs.lib()
+    sv, st, rho, idx = 1 << 40, (1 << 40) + (1 << 32), (1 << 40) + (2 << 32), (1 << 40) + (3 << 32)
+    assert L.trevs_spearman_workspace_size(2, 100, 30) > 0
+    assert L.trevs_spearman_workspace_size(2, 100, 101) == 0
+    ws = 1 << 44
+    need = L.trevs_spearman_workspace_size(2, 100, 30)
+    assert L.trevs_topk_spearman(sv, st, 2, 100, 101, rho, idx, ws, need, None) == 1
+    assert L.trevs_topk_spearman(sv, st, 2, 100, 0, rho, idx, ws, need, None) == 1
+    assert L.trevs_topk_spearman(None, st, 2, 100, 30, rho, idx, ws, need, None) == 1
+    assert L.trevs_topk_spearman(sv, st, 2, 100, 30, rho + 4, idx, ws, need, None) == 1
+    assert L.trevs_topk_spearman(sv, st, 2, 100, 30, sv + 8, idx, ws, need, None) == 1
+    assert L.trevs_topk_spearman(sv, st, 2, 40000, 30, rho, idx, ws, need, None) == 2
+    assert L.trevs_topk_spearman(sv, st, 2, 100, 30, rho, idx, ws, need - 1, None) == 3
+    assert L.trevs_topk_spearman(sv, st, 2, 100, 30, rho, idx, None, 0, None) == 3
