@@ -22,7 +22,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}  # dense matrix-core peaks of the compute type
 METRIC = "visual tokens scored+pruned/sec (both stages) at 1 MI355X; % of HBM roofline"
+ANALYSIS_METRIC = ("analysis samples/sec (text sensitivity of every head for two questions, "
+                   "Eq. 1, + Spearman of s^v and s^t in the top-K1 saliency set) at 1 MI355X")
 
 
 def algorithmic_bytes(w, text_len):
@@ -89,6 +92,139 @@ def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights", k_div=0):
                       f"{el:.1f} s"}
 
 
+def profile_flops(w, text_len):
+    """Matrix flops of one profile launch (one question): the logits of the
+    valid text rows of every query head against the K1 visual keys."""
+    return 2.0 * float(np.sum(text_len)) * w.H_q * w.K1 * w.d_h
+
+
+def cpu_baseline_analysis(w, si, sv, st, budget_s):
+    """The CPU oracle on single samples of the analysis workload."""
+    import oracle
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        b = n % w.B
+        oracle.sensitivity(si["q0"][b:b + 1], si["k"][b:b + 1], si["q1"][b:b + 1], si["k"][b:b + 1],
+                           si["text_len0"][b:b + 1], si["text_len1"][b:b + 1], w.dtype, P=w.P,
+                           K1=w.K1, scale=1.0 / math.sqrt(w.d_h))
+        oracle.topk_saliency_spearman(sv[b].astype(np.float64), st[b].astype(np.float64), w.K1)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or n >= 4 * w.B:
+            break
+    return {"value": n / el, "unit": "samples/s", "cores": len(os.sched_getaffinity(0)),
+            "kind": "oracle",
+            "sample": f"{n} single samples (B=1) of the analysis on {w.name}, float64 NumPy, {el:.1f} s"}
+
+
+def run_analysis(args, w):
+    """One step = trevs_text_sensitivity (two questions at the stage-2 shape)
+    + trevs_topk_spearman (top-K1 of the stage-1 scores), inputs in HBM."""
+    import torch
+
+    from paper_2609_37581_amd import trevs
+    from synthetic import sensitivity_inputs, stage1_inputs
+
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating the analysis inputs of {w.name}", file=sys.stderr, flush=True)
+    si = sensitivity_inputs(w)
+    s1 = stage1_inputs(w)
+
+    def to_dev(a):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        return (t.view(torch.bfloat16) if t.dtype == torch.uint16 else t).to(dev)
+
+    q0, q1, k = to_dev(si["q0"]), to_dev(si["q1"]), to_dev(si["k"])
+    tl0, tl1 = to_dev(si["text_len0"]), to_dev(si["text_len1"])
+    sens = trevs.TextSensitivity(q0, k, q1, k, tl0, tl1, P=w.P, K_in=w.K1)
+    # s^v and s^t from the library's stage 1 (outside the timed region)
+    pre = trevs.Prellm(to_dev(s1["cls_logits"]), to_dev(s1["vis_feats"]), to_dev(s1["text_emb"]),
+                       to_dev(s1["text_len"]), k_keep=w.K1, n_seg=w.n_seg, want_scores=True)
+    pre()
+    spear = trevs.TopkSpearman(pre.sal, pre.rel, w.K1)
+    stream = torch.cuda.current_stream()
+    nk = 2 * trevs.SENSITIVITY_NUM_KERNELS
+    per = nk + 2
+    ev = trevs.HipEvents(args.steps * per)
+
+    def step(i=None, all_events=False):
+        if i is None:
+            sens(stream)
+            spear(stream)
+            return
+        base = i * per
+        if all_events:
+            sens(stream, events=ev.handles[base:base + nk])
+        else:
+            # profile launches of both questions only (slots 4,5 and 10,11)
+            e = [None] * nk
+            for j in (4, 5, 10, 11):
+                e[j] = ev.handles[base + j]
+            sens(stream, events=e)
+        if all_events:
+            ev.record(base + nk, stream)
+        spear(stream)
+        if all_events:
+            ev.record(base + nk + 1, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        step(i)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = start.elapsed_time(stop) / args.steps
+    prof_ms = [sum(ev.elapsed_ms(i * per + a, i * per + a + 1) for i in range(args.steps)) / args.steps
+               for a in (4, 10)]
+    nb_steps = min(args.steps, 20)
+    for i in range(nb_steps):
+        step(i, all_events=True)
+    torch.cuda.synchronize()
+    names = list(trevs.SENSITIVITY_KERNELS) + ["topk_spearman"]
+    kern_ms = {n: 0.0 for n in names}
+    for i in range(nb_steps):
+        for j, n in enumerate(names):
+            kern_ms[n] += ev.elapsed_ms(i * per + 2 * j, i * per + 2 * j + 1) / nb_steps
+    ev.close()
+
+    flops = [profile_flops(w, si["text_len0"]), profile_flops(w, si["text_len1"])]
+    achieved = (flops[0] + flops[1]) / ((prof_ms[0] + prof_ms[1]) * 1e-3) / 1e12
+    peak = MFMA_PEAK_TFLOPS[w.dtype]
+    result = {
+        "metric": ANALYSIS_METRIC,
+        "value": w.B / (ms_step * 1e-3),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}-analysis", "B": w.B, "N": w.N, "K1": w.K1,
+                   "T_max": w.T_max, "H_q": w.H_q, "H_kv": w.H_kv, "d_head": w.d_h},
+        "roofline": {"bound": "mfma", "kernel": "analysis.profile", "achieved": achieved,
+                     "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                     "flops_per_launch": flops},
+        "profile_us": [m * 1e3 for m in prof_ms],
+        "kernels_us_separate_pass": {n: round(v * 1e3, 3) for n, v in kern_ms.items()},
+        "wall_s": t_wall,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline_analysis(w, si, pre.sal.cpu().numpy(),
+                                                       pre.rel.cpu().numpy(), args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,6 +237,8 @@ def main():
                     help="farthest-point diversity tokens K_d within K1 (default 0: all pivots)")
     ap.add_argument("--ratio-mode", default="weights", choices=["weights", "budget"],
                     help="textual ratio as Eq. (7) branch weights (default) or as a budget split")
+    ap.add_argument("--analysis", action="store_true",
+                    help="time the Sec. 3 diagnostics (text sensitivity + Spearman) instead")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the pruning path "
@@ -114,6 +252,9 @@ def main():
     from synthetic import DEFAULT_BENCH_WORKLOAD, WORKLOADS, stage1_inputs, stage2_inputs
 
     w = WORKLOADS[args.workload or DEFAULT_BENCH_WORKLOAD]
+    if args.analysis:
+        run_analysis(args, w)
+        return
     dev = torch.device("cuda:0")
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     s1 = stage1_inputs(w)

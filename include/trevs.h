@@ -59,6 +59,7 @@ typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
 #define TREVS_MAX_SELECT_N 32768 /* tokens ranked per sample by one top-K */
 #define TREVS_PRELLM_NUM_KERNELS 5 /* prep, relevance, robust stats, fuse+top-K (+ diversity set), gather */
 #define TREVS_INLLM_NUM_KERNELS 5  /* t2v stats, head variance, head set+token score, top-K, compaction */
+#define TREVS_SENSITIVITY_NUM_KERNELS 7 /* per question: t2v stats, head variance, profile; then Eq. (1) */
 
 /* ------------------------------------------------------------------------
  * Stage 1 (pre-LLM), Sec. 4.1.  Per sample b:
@@ -204,6 +205,7 @@ typedef struct trevs_sensitivity_args {
   float* ts;                 /* OUT [B,H_q] text sensitivity */
   float* profile[2];         /* OPTIONAL OUT per question [B,H_q,K_in] s^c_h */
   float* head_var[2];        /* OPTIONAL OUT per question [B,H_q] u_h */
+  void* const* events;       /* OPTIONAL [2*TREVS_SENSITIVITY_NUM_KERNELS] hipEvent_t */
 } trevs_sensitivity_args;
 
 size_t trevs_sensitivity_workspace_size(const trevs_sensitivity_args* args);

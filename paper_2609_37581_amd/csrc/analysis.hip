@@ -10,68 +10,85 @@ namespace trevs {
 // ---------------------------------------------------------------------------
 // Visual profile of one head: profile[i] = (1/T_b) sum_{q<T_b} A[h,q,i] with
 // A the text->vision attention of the statistics pass (its row log-sum-exps
-// come in through lse2).  A workgroup owns V visual tokens of one (sample,
-// query head); workgroups of one (sample, KV head) are numbered
-// consecutively and mapped onto one XCD, so the key tile they share stays in
-// that L2.  The key tile sits in LDS; wave w takes the 32-row text blocks
-// w, w+QW, ..., recomputes the logits on the matrix cores (operand A = text
-// rows, operand B = key rows), turns them into attention and sums them
-// in-lane over its text rows.  The two half-waves and the waves are then
-// summed through LDS.
+// come in through lse2).  A workgroup owns one (sample, query head) and one
+// split of the visual keys; workgroups of one (sample, KV head) are numbered
+// consecutively and mapped onto one XCD, so the keys the group's query heads
+// share stay in that L2.  Wave w keeps the Q rows of text block w (of the
+// current pass) resident as MFMA operand A; the 32-key tiles of the split
+// stream through a ring of register stages into two alternating LDS buffers
+// and are read by every wave as operand B, so a lane's 16 accumulators are
+// 16 text rows of one visual column.  Each wave turns them into attention,
+// sums its rows in-lane and across the half-waves, and parks the column sums
+// in LDS; after the tile's barrier the first 32 threads add the waves' sums
+// in a fixed order into the split's running column sums (deterministic).
 // ---------------------------------------------------------------------------
+// Key tiles in flight: about eight 16-byte vectors per thread in registers.
+constexpr int profile_ring(int vectors_per_tile) {
+  return vectors_per_tile >= 8 ? 1 : (vectors_per_tile >= 4 ? 2 : 8 / vectors_per_tile);
+}
+
 template <class In, int DH, int QW>
 __global__ __launch_bounds__(64 * QW) void t2v_profile_kernel(ProfileArgs a) {
   constexpr int ROWB = DH * In::kBytes;
   constexpr int HALFB = ROWB / 2;
   constexpr int NF = HALFB / 64;
   constexpr int NT = 64 * QW;
-  constexpr int VB = ROWB <= 256 ? 2 : 1;  // 32-token blocks per workgroup
-  constexpr int V = 32 * VB;
   constexpr int LROW = ROWB + 16;
   constexpr int CPR = ROWB / 16;
-  constexpr int TV = V * CPR;
+  constexpr int TV = 32 * CPR;  // 16-byte vectors of one key tile
   constexpr int TVT = (TV + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) uint8_t klds[V * LROW];
-  __shared__ float red[QW][V];
+  constexpr int RING = profile_ring(TVT);
+  __shared__ __attribute__((aligned(16))) uint8_t klds[2][32 * LROW];
+  __shared__ float red[2][QW][32];
+  __shared__ float colsum[kProfileSplitMax];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
-  const int hl = lin % a.G;
-  const int tile = (lin / a.G) % a.n_vtiles;
-  const int bg = lin / (a.G * a.n_vtiles);
+  const int split = lin % a.n_split;
+  const int hl = (lin / a.n_split) % a.G;
+  const int bg = lin / (a.n_split * a.G);
   const int g = bg % a.H_kv, b = bg / a.H_kv;
-  const int h = g * a.G + hl, i0 = tile * V;
+  const int h = g * a.G + hl;
   const size_t seq0 = (size_t)b * a.S;
+  const int i_begin = split * a.split_len;
+  const int i_end = min(a.K_in, i_begin + a.split_len);
+  const int n_tiles = (i_end - i_begin + 31) / 32;
+  for (int t = tid; t < n_tiles * 32; t += NT) colsum[t] = 0.f;
 
-  // key rows i0..i0+V-1 of KV head g (rows past K_in re-read the last row)
-  {
-    const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) + (seq0 + a.P) * a.H_kv * ROWB +
-                           (size_t)g * ROWB;
-    const size_t kstride = (size_t)a.H_kv * ROWB;
-    u32x4 kv[TVT];
+  const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) + (seq0 + a.P) * a.H_kv * ROWB +
+                         (size_t)g * ROWB;
+  const size_t kstride = (size_t)a.H_kv * ROWB;
+  // one key tile (rows ib..ib+31) into registers; rows past the split re-read
+  // row i_begin (valid, cached)
+  auto load_tile = [&](int ib, u32x4 (&dst)[TVT]) {
 #pragma unroll
     for (int k = 0; k < TVT; ++k) {
       const int v = min(tid + k * NT, TV - 1), row = v / CPR, c = v - row * CPR;
-      kv[k] = ldg16(kbase + (size_t)min(i0 + row, a.K_in - 1) * kstride + c * 16);
+      const int i = ib + row;
+      dst[k] = ldg16(kbase + (size_t)(i < i_end ? i : i_begin) * kstride + c * 16);
     }
+  };
+  auto store_tile = [&](int buf, const u32x4 (&src)[TVT]) {
 #pragma unroll
     for (int k = 0; k < TVT; ++k) {
       const int v = tid + k * NT;
       if (v < TV) {
         const int row = v / CPR, c = v - row * CPR;
-        *reinterpret_cast<u32x4*>(&klds[row * LROW + c * 16]) = kv[k];
+        *reinterpret_cast<u32x4*>(&klds[buf][row * LROW + c * 16]) = src[k];
       }
     }
-  }
-  __syncthreads();
+  };
 
   const int Tb = a.text_len ? a.text_len[b] : a.T_max;
   const int n_qblk = (Tb + 31) / 32;
-  float tot[VB];
-#pragma unroll
-  for (int vb = 0; vb < VB; ++vb) tot[vb] = 0.f;
-  for (int qb = wave; qb < n_qblk; qb += QW) {
-    const int qrow = min(qb * 32 + col, a.T_max - 1);
+  const int n_pass = (n_qblk + QW - 1) / QW;  // uniform over the workgroup (barriers below)
+  const int n_iter = (n_tiles + RING - 1) / RING;
+  for (int pass = 0; pass < n_pass; ++pass) {
+    // text block of this wave; a wave past the last block reads a valid block
+    // and masks every row
+    const int qb = pass * QW + wave;
+    const int qbc = min(qb, n_qblk - 1);
+    const int qrow = min(qbc * 32 + col, a.T_max - 1);
     const uint8_t* qp = reinterpret_cast<const uint8_t*>(a.q) +
                         ((seq0 + a.P + a.K_in + qrow) * a.H_q + h) * ROWB + half * HALFB;
     u32x4 qf[NF][4];
@@ -81,51 +98,71 @@ __global__ __launch_bounds__(64 * QW) void t2v_profile_kernel(ProfileArgs a) {
       for (int j = 0; j < 4; ++j) qf[f][j] = ldg16(qp + f * 64 + j * 16);
     // rows of lse2 are padded to a multiple of 32: the block's reads stay in
     // the row; entries past T_b are masked below
-    const float* lrow = a.lse2 + ((size_t)b * a.H_q + h) * a.T_pad + qb * 32 + 4 * half;
-    float4 lse[4];
+    const float* lrow = a.lse2 + ((size_t)b * a.H_q + h) * a.T_pad + qbc * 32 + 4 * half;
+    float nl[16];  // minus the row log-sum-exp, or -inf for a masked row
 #pragma unroll
-    for (int j = 0; j < 4; ++j) lse[j] = *reinterpret_cast<const float4*>(lrow + 8 * j);
+    for (int j = 0; j < 4; ++j) {
+      const float4 l = *reinterpret_cast<const float4*>(lrow + 8 * j);
+      const float l4[4] = {l.x, l.y, l.z, l.w};
 #pragma unroll
-    for (int vb = 0; vb < VB; ++vb) {
-      const uint8_t* p = &klds[(vb * 32 + col) * LROW + half * HALFB];
-      f32x16 acc;
+      for (int c = 0; c < 4; ++c)
+        nl[4 * j + c] = (qb * 32 + mfma_row(4 * j + c, half) < Tb) ? -l4[c] : -INFINITY;
+    }
+
+    u32x4 ring[RING][TVT];
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
+    for (int c = 0; c < RING; ++c) load_tile(i_begin + 32 * c, ring[c]);
+    for (int it = 0; it < n_iter; ++it) {
 #pragma unroll
-      for (int f = 0; f < NF; ++f) {
-        u32x4 kf[4];
+      for (int c = 0; c < RING; ++c) {
+        const int t = it * RING + c;
+        // LDS buffer (t % 2) was last read at tile t - 2, before every wave
+        // passed the barrier of tile t - 1
+        store_tile(t & 1, ring[c]);
+        load_tile(i_begin + 32 * (t + RING), ring[c]);
+        __syncthreads();
+        if (t < n_tiles) {
+          const uint8_t* p = &klds[t & 1][col * LROW + half * HALFB];
+          f32x16 acc;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kf[j] = *reinterpret_cast<const u32x4*>(p + f * 64 + j * 16);
-        acc = mfma_frag(qf[f], kf, acc, In{});
-      }
+          for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float l4[4] = {lse[j].x, lse[j].y, lse[j].z, lse[j].w};
+          for (int f = 0; f < NF; ++f) {
+            u32x4 kf[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(acc[4 * j + c], a.scale_log2e, -l4[c]));
-          tot[vb] += (qb * 32 + mfma_row(4 * j + c, half) < Tb) ? e : 0.f;
+            for (int j = 0; j < 4; ++j) kf[j] = *reinterpret_cast<const u32x4*>(p + f * 64 + j * 16);
+            acc = mfma_frag(qf[f], kf, acc, In{});
+          }
+          float sum = 0.f;
+#pragma unroll
+          for (int rr = 0; rr < 16; ++rr) sum += __builtin_amdgcn_exp2f(fmaf(acc[rr], a.scale_log2e, nl[rr]));
+          sum += __shfl_xor(sum, 32, 64);
+          if (half == 0) red[t & 1][wave][col] = sum;
+        }
+        // the sums parked at this tile are read after the next barrier, and
+        // red[t & 1] is written again only after the one after it
+        if (t >= 1 && t - 1 < n_tiles && tid < 32) {
+          float v = 0.f;
+#pragma unroll
+          for (int w = 0; w < QW; ++w) v += red[(t - 1) & 1][w][tid];
+          colsum[(t - 1) * 32 + tid] += v;
         }
       }
     }
-  }
-  // a lane's registers are text rows of visual column vb*32 + col; the two
-  // half-waves hold different rows of the same column
+    __syncthreads();
+    // the last tile's sums (every earlier one was added inside the loop)
+    const int tl = n_iter * RING - 1;
+    if (tl < n_tiles && tid < 32) {
+      float v = 0.f;
 #pragma unroll
-  for (int vb = 0; vb < VB; ++vb) {
-    const float t = tot[vb] + __shfl_xor(tot[vb], 32, 64);
-    if (half == 0) red[wave][vb * 32 + col] = t;
-  }
-  __syncthreads();
-  const float inv_t = 1.f / (float)Tb;
-  for (int t = tid; t < V; t += NT) {
-    if (i0 + t < a.K_in) {
-      float v = red[0][t];
-#pragma unroll
-      for (int w = 1; w < QW; ++w) v += red[w][t];
-      a.profile[((size_t)b * a.H_q + h) * a.K_in + i0 + t] = v * inv_t;
+      for (int w = 0; w < QW; ++w) v += red[tl & 1][w][tid];
+      colsum[tl * 32 + tid] += v;
     }
+    __syncthreads();
   }
+  const float inv_t = 1.f / (float)Tb;
+  float* out = a.profile + ((size_t)b * a.H_q + h) * a.K_in;
+  for (int t = tid; t < i_end - i_begin; t += NT) out[i_begin + t] = colsum[t] * inv_t;
 }
 
 // ---------------------------------------------------------------------------
@@ -188,9 +225,11 @@ __global__ __launch_bounds__(kSensThreads) void sensitivity_kernel(SensitivityAr
 // integer sums per sample and forms the ratio in double.
 // ---------------------------------------------------------------------------
 constexpr int kRankWaves = 16;
-constexpr int kRankChunk = 1024;
+constexpr int kRankThreads = 64 * kRankWaves;
+constexpr int kRankChunk = 4096;                  // (s^v, s^t) pairs staged in LDS per step
+constexpr int kRankPer = kRankChunk / kRankThreads;  // pairs each thread stages
 
-__global__ __launch_bounds__(64 * kRankWaves) void spearman_rank_kernel(SpearmanArgs a) {
+__global__ __launch_bounds__(kRankThreads) void spearman_rank_kernel(SpearmanArgs a) {
   __shared__ float2 vals[kRankChunk];
   __shared__ int cnt[4][kRankWaves][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -205,11 +244,23 @@ __global__ __launch_bounds__(64 * kRankWaves) void spearman_rank_kernel(Spearman
   int lv = 0, ev = 0, lt = 0, et = 0;
   for (int c0 = 0; c0 < K; c0 += kRankChunk) {
     const int n = min(kRankChunk, K - c0);
-    for (int j = tid; j < n; j += 64 * kRankWaves) {
-      const int jj = min(max(idx[c0 + j], 0), a.N - 1);
-      vals[j] = make_float2(sv[jj], st[jj]);
+    // every index load of the chunk first, then every value load
+    int jj[kRankPer];
+#pragma unroll
+    for (int e = 0; e < kRankPer; ++e) {
+      const int j = tid + e * kRankThreads;
+      jj[e] = j < n ? min(max(idx[c0 + j], 0), a.N - 1) : 0;
+    }
+    float2 v[kRankPer];
+#pragma unroll
+    for (int e = 0; e < kRankPer; ++e) v[e] = make_float2(sv[jj[e]], st[jj[e]]);
+#pragma unroll
+    for (int e = 0; e < kRankPer; ++e) {
+      const int j = tid + e * kRankThreads;
+      if (j < n) vals[j] = v[e];
     }
     __syncthreads();
+#pragma unroll 4
     for (int j = wave; j < n; j += kRankWaves) {
       const float2 p = vals[j];
       lv += p.x < vi ? 1 : 0;
@@ -255,18 +306,25 @@ __global__ __launch_bounds__(64 * kRankWaves) void spearman_rank_kernel(Spearman
   }
 }
 
-__global__ __launch_bounds__(64) void spearman_final_kernel(SpearmanArgs a, int B) {
-  const int b = blockIdx.x * 64 + threadIdx.x;
-  if (b >= B) return;
+// One wave per sample: the workgroups' integer sums, then the ratio.
+__global__ __launch_bounds__(64) void spearman_final_kernel(SpearmanArgs a) {
+  const int b = blockIdx.x, lane = threadIdx.x;
   long long s_vt = 0, s_vv = 0, s_tt = 0;
   const long long* p = a.part + (size_t)b * a.n_tiles * 4;
-  for (int t = 0; t < a.n_tiles; ++t) {
+  for (int t = lane; t < a.n_tiles; t += 64) {
     s_vt += p[4 * t];
     s_vv += p[4 * t + 1];
     s_tt += p[4 * t + 2];
   }
-  a.rho[b] = (s_vv == 0 || s_tt == 0) ? __builtin_nan("")
-                                      : (double)s_vt / sqrt((double)s_vv * (double)s_tt);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    s_vt += __shfl_xor(s_vt, o, 64);
+    s_vv += __shfl_xor(s_vv, o, 64);
+    s_tt += __shfl_xor(s_tt, o, 64);
+  }
+  if (lane == 0)
+    a.rho[b] = (s_vv == 0 || s_tt == 0) ? __builtin_nan("")
+                                        : (double)s_vt / sqrt((double)s_vv * (double)s_tt);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -277,7 +335,7 @@ static int profile_waves(int T_max) {
 
 template <class In, int DH>
 static void launch_profile_t(const ProfileArgs& a, hipStream_t s) {
-  const dim3 grid(a.B * a.H_q * a.n_vtiles);
+  const dim3 grid(a.B * a.H_q * a.n_split);
   switch (profile_waves(a.T_max)) {
     case 4: hipLaunchKernelGGL((t2v_profile_kernel<In, DH, 4>), grid, dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL((t2v_profile_kernel<In, DH, 2>), grid, dim3(128), 0, s, a); break;
@@ -309,8 +367,8 @@ hipError_t launch_sensitivity(const SensitivityArgs& a, int B, hipStream_t s) {
 }
 
 hipError_t launch_spearman(const SpearmanArgs& a, int B, hipStream_t s) {
-  hipLaunchKernelGGL(spearman_rank_kernel, dim3(a.n_tiles, B), dim3(64 * kRankWaves), 0, s, a);
-  hipLaunchKernelGGL(spearman_final_kernel, dim3((B + 63) / 64), dim3(64), 0, s, a, B);
+  hipLaunchKernelGGL(spearman_rank_kernel, dim3(a.n_tiles, B), dim3(kRankThreads), 0, s, a);
+  hipLaunchKernelGGL(spearman_final_kernel, dim3(B), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

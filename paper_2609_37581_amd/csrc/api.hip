@@ -631,7 +631,12 @@ trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* a, void* ws, s
   uint8_t* w = reinterpret_cast<uint8_t*>(ws);
   const int G = a->H_q / a->H_kv;
   const int T_pad = (int)lse_rows_padded(a->T_max);
-  const int tile = score_tile_tokens(a->dtype, a->d_head);
+  // profile splits: about 1024 workgroups, each split 128..kProfileSplitMax keys
+  int n_split = (int)std::min<int64_t>((1024 + (int64_t)a->B * a->H_q - 1) / ((int64_t)a->B * a->H_q),
+                                       (a->K_in + 127) / 128);
+  n_split = std::max(std::max(n_split, 1), (a->K_in + kProfileSplitMax - 1) / kProfileSplitMax);
+  const int split_len = ((a->K_in + n_split - 1) / n_split + 31) / 32 * 32;
+  n_split = (a->K_in + split_len - 1) / split_len;
   SensitivityArgs sa;
   sa.H_q = a->H_q;
   sa.K_in = a->K_in;
@@ -657,7 +662,9 @@ trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* a, void* ws, s
     ta.split_len = L.sp.split_len;
     ta.n_rgroups = L.sp.n_rgroups;
     ta.part = part;
+    TREVS_TRY(record(a->events, 6 * c + 0, s));
     TREVS_HIP(launch_stats(ta, a->dtype, a->d_head, s));
+    TREVS_TRY(record(a->events, 6 * c + 1, s));
     HeadArgs ha;
     ha.part = part;
     ha.B = a->B;
@@ -670,7 +677,9 @@ trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* a, void* ws, s
     ha.lse_rest = a->lse_rest[c];
     ha.lse2 = lse2;
     ha.head_var = head_var;
+    TREVS_TRY(record(a->events, 6 * c + 2, s));
     TREVS_HIP(launch_heads(ha, s));
+    TREVS_TRY(record(a->events, 6 * c + 3, s));
     ProfileArgs pa;
     pa.q = a->q[c];
     pa.k = a->k[c];
@@ -683,15 +692,20 @@ trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* a, void* ws, s
     pa.H_q = a->H_q;
     pa.H_kv = a->H_kv;
     pa.G = G;
-    pa.n_vtiles = (a->K_in + tile - 1) / tile;
+    pa.n_split = n_split;
+    pa.split_len = split_len;
     pa.scale_log2e = a->scale * kLog2e;
     pa.lse2 = lse2;
     pa.text_len = a->text_len[c];
     pa.profile = profile;
+    TREVS_TRY(record(a->events, 6 * c + 4, s));
     TREVS_HIP(launch_profile(pa, a->dtype, a->d_head, s));
+    TREVS_TRY(record(a->events, 6 * c + 5, s));
     sa.profile[c] = profile;
   }
+  TREVS_TRY(record(a->events, 12, s));
   TREVS_HIP(launch_sensitivity(sa, a->B, s));
+  TREVS_TRY(record(a->events, 13, s));
   return TREVS_OK;
 }
 

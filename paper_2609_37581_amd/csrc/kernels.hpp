@@ -107,12 +107,13 @@ struct ProfileArgs {
   const void* q;
   const void* k;
   int B, S, P, K_in, T_max, T_pad, H_q, H_kv, G;
-  int n_vtiles;              // workgroups per (sample, head)
+  int n_split, split_len;    // visual columns per workgroup (multiple of 32, <= kProfileSplitMax)
   float scale_log2e;
   const float* lse2;         // [B,H_q,T_pad] row log-sum-exp in log2 units
   const int32_t* text_len;
   float* profile;            // [B,H_q,K_in] mean attention over the valid text rows
 };
+constexpr int kProfileSplitMax = 2048;
 struct SensitivityArgs {
   const float* profile[2];   // [B,H_q,K_in] per question
   int H_q, K_in;

@@ -17,9 +17,12 @@ LIB_PATH = os.path.join(_HERE, "libtrevs.so")
 TREVS_F32, TREVS_BF16 = 0, 1
 PRELLM_NUM_KERNELS = 5
 INLLM_NUM_KERNELS = 5
+SENSITIVITY_NUM_KERNELS = 7
 MAX_SELECT_N = 32768
 PRELLM_KERNELS = ("prep", "relevance", "norm_stats", "fuse_topk", "gather")
 INLLM_KERNELS = ("t2v_stats", "head_var", "token_score", "topk", "compaction")
+SENSITIVITY_KERNELS = ("t2v_stats.0", "head_var.0", "profile.0", "t2v_stats.1", "head_var.1",
+                       "profile.1", "sensitivity")
 
 _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "workspace", 4: "hip error"}
 
@@ -68,7 +71,7 @@ class SensitivityArgs(ctypes.Structure):
                 ("d_head", c_int32), ("scale", c_float), ("dtype", c_int32),
                 ("q", c_void_p * 2), ("k", c_void_p * 2), ("text_len", c_void_p * 2),
                 ("lse_rest", c_void_p * 2), ("ts", c_void_p), ("profile", c_void_p * 2),
-                ("head_var", c_void_p * 2)]
+                ("head_var", c_void_p * 2), ("events", c_void_p)]
 
 
 _lib = None
@@ -389,9 +392,12 @@ class TextSensitivity:
             raise TrevsError(st, "trevs_text_sensitivity")
         self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
 
-    def __call__(self, stream=None):
+    def __call__(self, stream=None, events=None):
+        ev = _EventArray(events, SENSITIVITY_NUM_KERNELS)
+        self.args.events = ev.ptr
         st = lib().trevs_text_sensitivity(ctypes.byref(self.args), self.workspace.data_ptr(),
                                           self.workspace.numel(), _stream(stream))
+        self.args.events = None
         if st:
             raise TrevsError(st, "trevs_text_sensitivity")
         return self.ts
@@ -404,24 +410,40 @@ def text_sensitivity(q, k, q2, k2, text_len=None, text_len2=None, **kw):
     return call.ts, call.profile, call.head_var
 
 
+class TopkSpearman:
+    """Spearman correlation of s^v and s^t within the top-k saliency set of
+    each sample (Sec. 3), outputs and workspace allocated once.  sv, st
+    [B,N] fp32 on the device; call() enqueues it and returns (rho float64
+    [B], kept_idx int32 [B,k] ascending)."""
+
+    def __init__(self, sv, st, k):
+        _check(sv, "sv", sv.device, 2, torch.float32)
+        _check(st, "st", sv.device, 2, torch.float32)
+        if st.shape != sv.shape:
+            raise ValueError("sv and st must have one shape")
+        self.inputs = (sv, st)
+        self.B, self.N = sv.shape
+        self.k = k
+        self.rho = torch.empty(self.B, dtype=torch.float64, device=sv.device)
+        self.kept_idx = torch.empty((self.B, k), dtype=torch.int32, device=sv.device)
+        self.ws_bytes = lib().trevs_spearman_workspace_size(self.B, self.N, k)
+        self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=sv.device)
+
+    def __call__(self, stream=None):
+        sv, st = self.inputs
+        stat = lib().trevs_topk_spearman(sv.data_ptr(), st.data_ptr(), self.B, self.N, self.k,
+                                         self.rho.data_ptr(), self.kept_idx.data_ptr(),
+                                         self.workspace.data_ptr(), self.ws_bytes, _stream(stream))
+        if stat:
+            raise TrevsError(stat, "trevs_topk_spearman")
+        return self.rho, self.kept_idx
+
+
 def topk_spearman(sv, st, k, stream=None):
     """Spearman correlation of s^v and s^t within the top-k saliency set of
     each sample (Sec. 3).  sv, st [B,N] fp32 on the device.  Returns
     (rho float64 [B], kept_idx int32 [B,k] ascending)."""
-    _check(sv, "sv", sv.device, 2, torch.float32)
-    _check(st, "st", sv.device, 2, torch.float32)
-    if st.shape != sv.shape:
-        raise ValueError("sv and st must have one shape")
-    B, N = sv.shape
-    rho = torch.empty(B, dtype=torch.float64, device=sv.device)
-    idx = torch.empty((B, k), dtype=torch.int32, device=sv.device)
-    ws_bytes = lib().trevs_spearman_workspace_size(B, N, k)
-    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=sv.device)
-    stat = lib().trevs_topk_spearman(sv.data_ptr(), st.data_ptr(), B, N, k, rho.data_ptr(),
-                                     idx.data_ptr(), ws.data_ptr(), ws_bytes, _stream(stream))
-    if stat:
-        raise TrevsError(stat, "trevs_topk_spearman")
-    return rho, idx
+    return TopkSpearman(sv, st, k)(stream)
 
 
 # ---------------------------------------------------------------- HIP events
@@ -434,12 +456,18 @@ class HipEvents:
         self.rt.hipEventCreate.argtypes = [ctypes.POINTER(c_void_p)]
         self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), c_void_p, c_void_p]
         self.rt.hipEventDestroy.argtypes = [c_void_p]
+        self.rt.hipEventRecord.argtypes = [c_void_p, c_void_p]
         self.handles = []
         for _ in range(n):
             h = c_void_p()
             if self.rt.hipEventCreate(ctypes.byref(h)):
                 raise RuntimeError("hipEventCreate failed")
             self.handles.append(h.value)
+
+    def record(self, i, stream=None):
+        """Record event i on the stream (torch's current stream by default)."""
+        if self.rt.hipEventRecord(self.handles[i], _stream(stream)):
+            raise RuntimeError("hipEventRecord failed")
 
     def elapsed_ms(self, i, j):
         ms = ctypes.c_float()

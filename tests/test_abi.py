@@ -42,7 +42,7 @@ def test_struct_mirror_sizes():
     L = trevs.lib()
     assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 168
     assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 192
-    assert L.trevs_sensitivity_args_size() == ctypes.sizeof(trevs.SensitivityArgs) == 152
+    assert L.trevs_sensitivity_args_size() == ctypes.sizeof(trevs.SensitivityArgs) == 160
 
 
 def test_status_strings_and_keep_count():
