@@ -41,7 +41,9 @@ Readings where the paper is silent (each also listed in the design notes):
     head h // (H_q / H_kv)).
   * Eq. (8)/(9) softmax domain: the K_1 visual keys only, unless a per-row
     log-sum-exp of the non-visual keys ("lse_rest") is supplied, which gives
-    the full-sequence softmax restricted to the visual columns.
+    the full-sequence softmax restricted to the visual columns; or the whole
+    causal row computed from the sequence (softmax="causal": prefix keys,
+    visual keys and the text keys up to the row itself).
   * compaction keeps the prefix rows, the K_2 selected visual rows (ascending)
     and the text rows, and copies the original position ids unchanged.
   * Eq. (1) (analysis of Sec. 3): a head's visual-token attention
@@ -284,6 +286,26 @@ def t2v_attention(x, lse_rest=None):
     return np.exp(x - lse[..., None]), lse
 
 
+def causal_rest_lse(q, k, *, P, K1, T_b, scale):
+    """Log-sum-exp of each text row's non-visual logits over its causal row,
+    from the sequence itself (the full-sequence softmax of Sec. 4.2 read as
+    the model's causal attention at layer l*): text row t, at position
+    P+K1+t, sees the prefix rows [0, P) and the text rows P+K1 .. P+K1+t.
+    q [S, H_q, d_h], k [S, H_kv, d_h] float64 -> [H_q, T_b]."""
+    Hq = q.shape[1]
+    G = Hq // k.shape[1]
+    out = np.empty((Hq, T_b))
+    for h in range(Hq):
+        qt = q[P + K1:P + K1 + T_b, h, :]
+        kr = np.concatenate([k[:P, h // G, :], k[P + K1:P + K1 + T_b, h // G, :]])
+        x = scale * (qt @ kr.T)
+        for t in range(T_b):
+            x[t, P + t + 1:] = -np.inf
+        m = x.max(axis=1)
+        out[h] = m + np.log(np.exp(x - m[:, None]).sum(axis=1))
+    return out
+
+
 def head_variance(A):
     """Eq. (8): u_h = mean over text rows q of the population variance over
     the K_1 visual columns of A[h, q, :].  A: [H_q, T_b, K_1] -> u [H_q]."""
@@ -313,11 +335,17 @@ def compaction_rows(S, P, K1, kept):
 
 
 def inllm_sample(q, k, *, P, K1, T_b, n_keep, k_keep, scale, lse_rest=None,
-                 heads=None):
+                 heads=None, softmax="visual"):
     """Stage 2 scoring for one sample, inputs float64: q [S, H_q, d_h],
     k [S, H_kv, d_h] with visual rows [P, P+K1) and text rows
     [P+K1, P+K1+T_b).  `heads`, when given, replaces the selected head set
-    (used to score with another side's head choice).  Returns a dict."""
+    (used to score with another side's head choice).  softmax="causal" takes
+    each text row's softmax over its whole causal row (causal_rest_lse)
+    instead of over the visual keys only.  Returns a dict."""
+    if softmax == "causal":
+        if lse_rest is not None:
+            raise ValueError("lse_rest is for the visual softmax domain only")
+        lse_rest = causal_rest_lse(q, k, P=P, K1=K1, T_b=T_b, scale=scale)
     x = t2v_logits(q[P + K1:P + K1 + T_b], k[P:P + K1], scale)
     A, lse = t2v_attention(x, lse_rest)
     u = head_variance(A)
@@ -328,7 +356,7 @@ def inllm_sample(q, k, *, P, K1, T_b, n_keep, k_keep, scale, lse_rest=None,
 
 
 def inllm(q, k, v, hidden, pos, text_len, dtype, *, P, K1, n_keep, k_keep,
-          scale, lse_rest=None, heads=None):
+          scale, lse_rest=None, heads=None, softmax="visual"):
     """Stage 2 over a batch.  q [B,S,H_q,d_h], k, v [B,S,H_kv,d_h],
     hidden [B,S,D] in storage form; pos int64 [n_pos,B,S]; text_len [B] or
     None (= T_max = S - P - K1).  Outputs the compacted tensors as bit copies
@@ -344,7 +372,7 @@ def inllm(q, k, v, hidden, pos, text_len, dtype, *, P, K1, n_keep, k_keep,
         r = inllm_sample(to_f64(q[b], dtype), to_f64(k[b], dtype), P=P, K1=K1,
                          T_b=tb, n_keep=n_keep, k_keep=k_keep, scale=scale,
                          lse_rest=None if lse_rest is None else lse_rest[b][:, :tb],
-                         heads=None if heads is None else heads[b])
+                         heads=None if heads is None else heads[b], softmax=softmax)
         for key in res:
             res[key].append(r[key])
         rows.append(compaction_rows(S, P, K1, r["kept_idx"]))
@@ -379,7 +407,7 @@ def text_sensitivity(s1, s2):
 
 
 def sensitivity_sample(q1, k1, q2, k2, *, P, K1, T1, T2, scale, lse_rest1=None,
-                       lse_rest2=None):
+                       lse_rest2=None, softmax="visual"):
     """Text sensitivity of every head for one image paired with two questions
     (Sec. 3, Eq. (1)).  Each question is a stage-2 input of the layout of
     inllm_sample (float64 q [S, H_q, d_h], k [S, H_kv, d_h]) with T1 / T2
@@ -387,6 +415,10 @@ def sensitivity_sample(q1, k1, q2, k2, *, P, K1, T1, T2, scale, lse_rest1=None,
     questions' head variances u_h of Eq. (8)."""
     out = {}
     for c, (q, k, tb, rest) in enumerate(((q1, k1, T1, lse_rest1), (q2, k2, T2, lse_rest2))):
+        if softmax == "causal":
+            if rest is not None:
+                raise ValueError("lse_rest is for the visual softmax domain only")
+            rest = causal_rest_lse(q, k, P=P, K1=K1, T_b=tb, scale=scale)
         x = t2v_logits(q[P + K1:P + K1 + tb], k[P:P + K1], scale)
         A, _ = t2v_attention(x, rest)
         out[f"profile{c}"] = visual_profile(A)
@@ -396,7 +428,7 @@ def sensitivity_sample(q1, k1, q2, k2, *, P, K1, T1, T2, scale, lse_rest1=None,
 
 
 def sensitivity(q1, k1, q2, k2, text_len1, text_len2, dtype, *, P, K1, scale,
-                lse_rest1=None, lse_rest2=None):
+                lse_rest1=None, lse_rest2=None, softmax="visual"):
     """Batch form of sensitivity_sample on storage-form inputs
     ([B, S, H, d_h]); text_len* [B] or None (= T_max = S - P - K1)."""
     B, S = q1.shape[:2]
@@ -412,7 +444,7 @@ def sensitivity(q1, k1, q2, k2, text_len1, text_len2, dtype, *, P, K1, scale,
             to_f64(q1[b], dtype), to_f64(k1[b], dtype), to_f64(q2[b], dtype), to_f64(k2[b], dtype),
             P=P, K1=K1, T1=t1, T2=t2, scale=scale,
             lse_rest1=None if lse_rest1 is None else lse_rest1[b][:, :t1],
-            lse_rest2=None if lse_rest2 is None else lse_rest2[b][:, :t2])
+            lse_rest2=None if lse_rest2 is None else lse_rest2[b][:, :t2], softmax=softmax)
         for key in keys:
             res[key].append(r[key])
     return {key: np.stack(val) for key, val in res.items()}

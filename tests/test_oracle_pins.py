@@ -448,3 +448,33 @@ def test_topk_saliency_spearman_brute_force():
             assert rho == pytest.approx(want, rel=1e-12, abs=1e-15)
         full, _ = oracle.topk_saliency_spearman(sv, st, N)
         assert full == pytest.approx(scipy.stats.spearmanr(sv, st)[0], rel=1e-12, abs=1e-15)
+
+
+@pytest.mark.parametrize("Hq,Hkv,P", [(4, 4, 3), (6, 2, 0)])
+def test_causal_softmax_matches_torch_masked_attention(Hq, Hkv, P):
+    """softmax="causal": the visual columns of each text row's softmax over
+    its whole causal row, against an independent float64 PyTorch causal
+    attention over the full sequence (GQA by repeat_interleave), and u_h and
+    p of Eq. (8)-(9) on those attention rows."""
+    K1, T, dh, scale = 13, 7, 8, 0.4
+    S = P + K1 + T + 2  # rows after the text are not attended by it
+    q = RNG.standard_normal((S, Hq, dh))
+    k = RNG.standard_normal((S, Hkv, dh))
+    Tb = 5
+    qt = torch.from_numpy(q).permute(1, 0, 2)
+    kt = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(Hq // Hkv, dim=0)
+    x = scale * qt @ kt.transpose(1, 2)
+    pos = torch.arange(S)
+    x = x.masked_fill(pos[None, :] > pos[:, None], float("-inf"))
+    A_full = torch.softmax(x, dim=-1)[:, P + K1:P + K1 + Tb, P:P + K1].numpy()
+    r = oracle.inllm_sample(q, k, P=P, K1=K1, T_b=Tb, n_keep=2, k_keep=4, scale=scale,
+                            softmax="causal")
+    u = ((A_full - A_full.mean(-1, keepdims=True)) ** 2).mean(-1).mean(-1)
+    np.testing.assert_allclose(r["head_var"], u, rtol=1e-10)
+    p = (A_full[r["head_sel"]].sum(0) / 2).max(0)
+    np.testing.assert_allclose(r["score"], p, rtol=1e-10)
+    rest = oracle.causal_rest_lse(q, k, P=P, K1=K1, T_b=Tb, scale=scale)
+    A, _ = oracle.t2v_attention(oracle.t2v_logits(q[P + K1:P + K1 + Tb], k[P:P + K1], scale), rest)
+    np.testing.assert_allclose(A, A_full, rtol=1e-11)
+    # each row's attention over the visual block sums to less than 1
+    assert (A.sum(-1) < 1).all()
