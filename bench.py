@@ -28,9 +28,11 @@ ANALYSIS_METRIC = ("analysis samples/sec (text sensitivity of every head for two
                    "Eq. 1, + Spearman of s^v and s^t in the top-K1 saliency set) at 1 MI355X")
 
 
-def algorithmic_bytes(w, text_len):
+def algorithmic_bytes(w, text_len, softmax="visual"):
     """Bytes the method must move per step (every input read once, every
-    output written once) and per launch of the relevance kernel."""
+    output written once) and per launch of the relevance kernel.  The causal
+    softmax domain also reads each text row's non-visual keys (prefix and
+    text rows of K)."""
     e = w.elem_bytes
     B = w.B
     m_bar = float(np.mean(text_len))
@@ -39,6 +41,8 @@ def algorithmic_bytes(w, text_len):
     So = w.S - w.K1 + w.K2
     stage2 = (B * e * (m_bar * w.H_q * w.d_h + w.K1 * w.H_kv * w.d_h)
               + B * (2 * So * w.D * e + 4 * So * w.H_kv * w.d_h * e + 2 * w.n_pos * So * 8 + 4 * w.K2))
+    if softmax == "causal":
+        stage2 += B * e * (w.P + m_bar) * w.H_kv * w.d_h
     return dict(relevance=rel, stage1=stage1, stage2=stage2, total=stage1 + stage2)
 
 
@@ -64,7 +68,7 @@ def counter_traffic(workload):
     return float(vals["hbm_bytes_per_launch"])
 
 
-def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights", k_div=0):
+def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights", k_div=0, softmax="visual"):
     """The CPU oracle as it stands, on single samples of the same workload,
     repeated until about budget_s seconds of work."""
     import oracle
@@ -82,10 +86,10 @@ def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights", k_div=0):
                       ratio_mode=ratio_mode, k_div=k_div)
         oracle.inllm(s2["q"][b:b + 1], s2["k"][b:b + 1], s2["v"][b:b + 1], s2["hidden"][b:b + 1],
                      s2["pos"][:, b:b + 1], s2["text_len"][b:b + 1], w.dtype, P=w.P, K1=w.K1,
-                     n_keep=w.n_keep, k_keep=w.K2, scale=1.0 / math.sqrt(w.d_h))
+                     n_keep=w.n_keep, k_keep=w.K2, scale=1.0 / math.sqrt(w.d_h), softmax=softmax)
         n += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or n >= 4 * w.B:
+        if el >= budget_s:
             break
     return {"value": n * w.N / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{n} single samples (B=1) of {w.name}, both stages, float64 NumPy, "
@@ -111,7 +115,7 @@ def cpu_baseline_analysis(w, si, sv, st, budget_s):
         oracle.topk_saliency_spearman(sv[b].astype(np.float64), st[b].astype(np.float64), w.K1)
         n += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or n >= 4 * w.B:
+        if el >= budget_s:
             break
     return {"value": n / el, "unit": "samples/s", "cores": len(os.sched_getaffinity(0)),
             "kind": "oracle",
@@ -237,6 +241,9 @@ def main():
                     help="farthest-point diversity tokens K_d within K1 (default 0: all pivots)")
     ap.add_argument("--ratio-mode", default="weights", choices=["weights", "budget"],
                     help="textual ratio as Eq. (7) branch weights (default) or as a budget split")
+    ap.add_argument("--softmax", default="visual", choices=["visual", "causal"],
+                    help="stage-2 softmax over the visual keys (default) or each text row's "
+                         "whole causal row")
     ap.add_argument("--analysis", action="store_true",
                     help="time the Sec. 3 diagnostics (text sensitivity + Spearman) instead")
     args = ap.parse_args()
@@ -271,7 +278,7 @@ def main():
     pre = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, n_seg=w.n_seg, textual_ratio=w.rho,
                        ratio_mode=args.ratio_mode, k_div=args.k_div)
     inl = trevs.Inllm(q, k, v, hid, pos, tl2, P=w.P, K_in=w.K1, n_keep_heads=w.n_keep,
-                      k_keep=w.K2)
+                      k_keep=w.K2, softmax=args.softmax)
     stream = torch.cuda.current_stream()
     n1, n2 = 2 * trevs.PRELLM_NUM_KERNELS, 2 * trevs.INLLM_NUM_KERNELS
     ev = trevs.HipEvents(args.steps * (n1 + n2))
@@ -336,7 +343,7 @@ def main():
     copy_gbps = 2 * nbytes * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del src, dst
 
-    nb = algorithmic_bytes(w, s1["text_len"])
+    nb = algorithmic_bytes(w, s1["text_len"], args.softmax)
     traffic = counter_traffic(w.name)
     rel_s = rel_ms * 1e-3
     achieved = nb["relevance"] / rel_s / 1e9
@@ -355,7 +362,8 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "ratio_mode": args.ratio_mode, "k_div": args.k_div, "B": w.B, "N": w.N, "d": w.d, "M_max": w.M_max,
+        "config": {"workload": w.name, "ratio_mode": args.ratio_mode, "k_div": args.k_div,
+                   "softmax": args.softmax, "B": w.B, "N": w.N, "d": w.d, "M_max": w.M_max,
                    "K1": w.K1, "K2": w.K2, "H_q": w.H_q, "H_kv": w.H_kv, "d_head": w.d_h,
                    "D": w.D, "n_keep_heads": w.n_keep, "P": w.P, "S": w.S},
         "roofline": {"bound": "hbm", "kernel": "prellm.relevance", "achieved": achieved,
@@ -370,7 +378,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(w, s1, s2, args.cpu_seconds, args.ratio_mode, args.k_div)
+        result["cpu_baseline"] = cpu_baseline(w, s1, s2, args.cpu_seconds, args.ratio_mode, args.k_div,
+                                              args.softmax)
     print(json.dumps(result), flush=True)
 
 

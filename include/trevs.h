@@ -58,7 +58,7 @@ typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
 /* Implementation limits (TREVS_ERR_UNSUPPORTED beyond them). */
 #define TREVS_MAX_SELECT_N 32768 /* tokens ranked per sample by one top-K */
 #define TREVS_PRELLM_NUM_KERNELS 5 /* prep, relevance, robust stats, fuse+top-K (+ diversity set), gather */
-#define TREVS_INLLM_NUM_KERNELS 5  /* t2v stats, head variance, head set+token score, top-K, compaction */
+#define TREVS_INLLM_NUM_KERNELS 5  /* t2v stats (+ causal rest keys), head variance, head set+token score, top-K, compaction */
 #define TREVS_SENSITIVITY_NUM_KERNELS 7 /* per question: t2v stats, head variance, profile; then Eq. (1) */
 
 /* ------------------------------------------------------------------------
@@ -131,9 +131,18 @@ typedef struct trevs_prellm_args {
  * then any further rows up to S.  Per sample b with G = H_q/H_kv and
  * T_b = text_len[b]:
  *   x[h,q,i] = scale * q[b,P+K_in+q,h,:] . k[b,P+i,h/G,:]   (q < T_b, i < K_in)
- *   A[h,q,:] = exp(x[h,q,:] - LSE[h,q]), LSE = logsumexp_i x[h,q,i], or, when
- *              lse_rest is given, logaddexp(that, lse_rest[b,h,q]): the
- *              full-row softmax restricted to the visual columns.
+ *   A[h,q,:] = exp(x[h,q,:] - LSE[h,q]) over the visual columns, where the
+ *              softmax domain (trevs_softmax) sets LSE[h,q]:
+ *              VISUAL: logsumexp_i x[h,q,i] over the K_in visual keys; when
+ *                lse_rest is given, logaddexp(that, lse_rest[b,h,q]), the
+ *                full-row softmax with the non-visual part supplied by the
+ *                caller;
+ *              CAUSAL: the log-sum-exp of the row's whole causal attention
+ *                row at this layer, computed from q and k: the prefix keys
+ *                [0,P), the visual keys, and the text keys P+K_in .. P+K_in+q
+ *                (the row's own position and those before it); every key
+ *                uses the row's KV head h/G.  A thus holds the visual columns
+ *                of the layer's own attention matrix (Sec. 4.2).
  *   u_h      = (1/T_b) sum_q Var_i A[h,q,i]  (population variance)    Eq. (8)
  *   H*       = the n_keep_heads heads first under (u desc, h asc)
  *   p_i      = max_{q<T_b} (1/|H*|) sum_{h in H*} A[h,q,i]            Eq. (9)
@@ -142,6 +151,11 @@ typedef struct trevs_prellm_args {
  *   hidden_out[b] = hidden[b,rows], k_out[b] = k[b,rows], v_out[b] = v[b,rows],
  *   pos_out[p,b]  = pos[p,b,rows]   (bit copies; position ids are not renumbered)
  * ---------------------------------------------------------------------- */
+typedef enum trevs_softmax {
+  TREVS_SOFTMAX_VISUAL = 0,  /* softmax over the visual keys (plus lse_rest, if given) */
+  TREVS_SOFTMAX_CAUSAL = 1   /* softmax over each text row's causal row of the sequence */
+} trevs_softmax;
+
 typedef struct trevs_inllm_args {
   uint32_t struct_size;      /* sizeof(trevs_inllm_args) */
   int32_t B;                 /* samples */
@@ -163,7 +177,8 @@ typedef struct trevs_inllm_args {
   const void* hidden;        /* [B,S,D] (16-byte aligned) */
   const int64_t* pos;        /* [n_pos,B,S] */
   const int32_t* text_len;   /* [B] T_b in 1..T_max, or NULL (= T_max) */
-  const float* lse_rest;     /* OPTIONAL [B,H_q,T_max] log-sum-exp of each text row's non-visual logits */
+  const float* lse_rest;     /* OPTIONAL [B,H_q,T_max] log-sum-exp of each text row's non-visual
+                                logits (natural log); VISUAL softmax only, NULL with CAUSAL */
   int32_t* kept_idx;         /* OUT [B,k_keep] ascending, relative to the visual block */
   void* hidden_out;          /* OUT [B,S',D] (16-byte aligned) */
   void* k_out;               /* OUT [B,S',H_kv,d_head] (16-byte aligned) */
@@ -173,6 +188,7 @@ typedef struct trevs_inllm_args {
   float* head_var;           /* OPTIONAL OUT [B,H_q] u_h */
   float* score_out;          /* OPTIONAL OUT [B,K_in] p_i */
   void* const* events;       /* OPTIONAL [2*TREVS_INLLM_NUM_KERNELS] hipEvent_t */
+  int32_t softmax;           /* trevs_softmax: domain of the attention softmax (0 = VISUAL) */
 } trevs_inllm_args;
 
 /* ------------------------------------------------------------------------
@@ -183,8 +199,9 @@ typedef struct trevs_inllm_args {
  * two questions gives two stage-2 inputs of one shape, each laid out as for
  * trevs_inllm_prune (visual rows [P,P+K_in), text rows after them).  For
  * question c in {0,1} with T^c_b = text_len[c][b] valid text rows:
- *   A^c[h,q,:]  = the text->vision attention of trevs_inllm_prune (visual-only
- *                 softmax, or the full row when lse_rest[c] is given)
+ *   A^c[h,q,:]  = the text->vision attention of trevs_inllm_prune, in the
+ *                 same softmax domain (VISUAL, with lse_rest[c] if given, or
+ *                 CAUSAL computed from q[c] and k[c])
  *   s^c_h       = (1/T^c_b) sum_{q<T^c_b} A^c[h,q,:]   the head's attention
  *                 distribution over the visual tokens for that question
  *   ts[b,h]     = 1 - cos(s^0_h, s^1_h)                                 Eq. (1)
@@ -201,11 +218,13 @@ typedef struct trevs_sensitivity_args {
   const void* q[2];          /* per question [B,S,H_q,d_head] (16-byte aligned) */
   const void* k[2];          /* per question [B,S,H_kv,d_head] (16-byte aligned); may be one buffer */
   const int32_t* text_len[2];  /* per question [B] in 1..T_max, or NULL (= T_max) */
-  const float* lse_rest[2];  /* OPTIONAL per question [B,H_q,T_max] non-visual log-sum-exp */
+  const float* lse_rest[2];  /* OPTIONAL per question [B,H_q,T_max] non-visual log-sum-exp
+                                (VISUAL softmax only) */
   float* ts;                 /* OUT [B,H_q] text sensitivity */
   float* profile[2];         /* OPTIONAL OUT per question [B,H_q,K_in] s^c_h */
   float* head_var[2];        /* OPTIONAL OUT per question [B,H_q] u_h */
   void* const* events;       /* OPTIONAL [2*TREVS_SENSITIVITY_NUM_KERNELS] hipEvent_t */
+  int32_t softmax;           /* trevs_softmax, as in trevs_inllm_args (0 = VISUAL) */
 } trevs_sensitivity_args;
 
 size_t trevs_sensitivity_workspace_size(const trevs_sensitivity_args* args);

@@ -137,8 +137,8 @@ PrellmLayout prellm_layout(const trevs_prellm_args* a) {
 
 // ------------------------------------------------------------------ stage 2
 struct InllmPlan {
-  int n_split, split_len, n_rgroups;
-  size_t part, lse2, head_var, head_sel, score, total;
+  int n_split, split_len, n_rgroups, rest_len;
+  size_t part, part_rest, lse2, head_var, head_sel, score, total;
 };
 
 trevs_status validate_inllm(const trevs_inllm_args* a) {
@@ -153,6 +153,8 @@ trevs_status validate_inllm(const trevs_inllm_args* a) {
   if (a->n_keep_heads < 1 || a->n_keep_heads > a->H_q) return TREVS_ERR_INVALID_ARG;
   if (a->k_keep < 1 || a->k_keep > a->K_in) return TREVS_ERR_INVALID_ARG;
   if (!finite(a->scale) || a->scale <= 0.f) return TREVS_ERR_INVALID_ARG;
+  if (a->softmax != TREVS_SOFTMAX_VISUAL && a->softmax != TREVS_SOFTMAX_CAUSAL) return TREVS_ERR_INVALID_ARG;
+  if (a->softmax == TREVS_SOFTMAX_CAUSAL && a->lse_rest) return TREVS_ERR_INVALID_ARG;
   if (!a->q || !a->k || !a->v || !a->hidden || !a->pos || !a->kept_idx || !a->hidden_out ||
       !a->k_out || !a->v_out || !a->pos_out)
     return TREVS_ERR_INVALID_ARG;
@@ -194,8 +196,9 @@ trevs_status validate_inllm(const trevs_inllm_args* a) {
 // (the pass consumes key tiles in pairs of 32).
 struct StatsPlan {
   int n_split, split_len, n_rgroups;
+  int rest_len;  // causal non-visual keys per split, multiple of 32 (0: visual-only softmax)
 };
-StatsPlan stats_plan(int B, int K_in, int T_max, int H_q, int H_kv) {
+StatsPlan stats_plan(int B, int K_in, int T_max, int H_q, int H_kv, int softmax, int P) {
   StatsPlan p;
   const int G = H_q / H_kv;
   const int nrb = (G * T_max + 31) / 32;
@@ -206,6 +209,8 @@ StatsPlan stats_plan(int B, int K_in, int T_max, int H_q, int H_kv) {
   n_split = std::max(n_split, 1);
   p.split_len = ((K_in + n_split - 1) / n_split + 63) / 64 * 64;
   p.n_split = (K_in + p.split_len - 1) / p.split_len;
+  // the causal non-visual keys (P prefix + T_max text) shared evenly by the splits
+  p.rest_len = softmax == TREVS_SOFTMAX_CAUSAL ? ((P + T_max + p.n_split - 1) / p.n_split + 31) / 32 * 32 : 0;
   return p;
 }
 
@@ -213,14 +218,17 @@ size_t lse_rows_padded(int T_max) { return (size_t)(T_max + 31) / 32 * 32; }
 
 InllmPlan inllm_plan(const trevs_inllm_args* a) {
   InllmPlan p;
-  const StatsPlan sp = stats_plan(a->B, a->K_in, a->T_max, a->H_q, a->H_kv);
+  const StatsPlan sp = stats_plan(a->B, a->K_in, a->T_max, a->H_q, a->H_kv, a->softmax, a->P);
   p.n_split = sp.n_split;
   p.split_len = sp.split_len;
   p.n_rgroups = sp.n_rgroups;
+  p.rest_len = sp.rest_len;
   const size_t rows = (size_t)a->B * a->H_q * a->T_max;
   size_t off = 0;
   p.part = off;
   off = align_up(off + rows * p.n_split * sizeof(float4));
+  p.part_rest = off;
+  off = align_up(off + (p.rest_len ? rows * p.n_split * sizeof(float4) : 0));
   p.lse2 = off;
   off = align_up(off + (size_t)a->B * a->H_q * lse_rows_padded(a->T_max) * sizeof(float));
   p.head_var = off;
@@ -241,6 +249,8 @@ trevs_status validate_sensitivity(const trevs_sensitivity_args* a) {
   if ((int64_t)a->P + a->K_in + a->T_max > a->S) return TREVS_ERR_INVALID_ARG;
   if (a->H_q < 1 || a->H_kv < 1 || a->H_q % a->H_kv || a->d_head < 1) return TREVS_ERR_INVALID_ARG;
   if (!finite(a->scale) || a->scale <= 0.f) return TREVS_ERR_INVALID_ARG;
+  if (a->softmax != TREVS_SOFTMAX_VISUAL && a->softmax != TREVS_SOFTMAX_CAUSAL) return TREVS_ERR_INVALID_ARG;
+  if (a->softmax == TREVS_SOFTMAX_CAUSAL && (a->lse_rest[0] || a->lse_rest[1])) return TREVS_ERR_INVALID_ARG;
   if (!a->ts || !aligned(a->ts, 4)) return TREVS_ERR_INVALID_ARG;
   const int e = elem_bytes(a->dtype);
   const size_t B = a->B, S = a->S;
@@ -268,17 +278,19 @@ trevs_status validate_sensitivity(const trevs_sensitivity_args* a) {
 
 struct SensitivityLayout {
   StatsPlan sp;
-  size_t part[2], lse2[2], head_var[2], profile[2], total;
+  size_t part[2], part_rest[2], lse2[2], head_var[2], profile[2], total;
 };
 
 SensitivityLayout sensitivity_layout(const trevs_sensitivity_args* a) {
   SensitivityLayout L;
-  L.sp = stats_plan(a->B, a->K_in, a->T_max, a->H_q, a->H_kv);
+  L.sp = stats_plan(a->B, a->K_in, a->T_max, a->H_q, a->H_kv, a->softmax, a->P);
   const size_t heads = (size_t)a->B * a->H_q;
   size_t off = 0;
   for (int c = 0; c < 2; ++c) {
     L.part[c] = off;
     off = align_up(off + heads * a->T_max * L.sp.n_split * sizeof(float4));
+    L.part_rest[c] = off;
+    off = align_up(off + (L.sp.rest_len ? heads * a->T_max * L.sp.n_split * sizeof(float4) : 0));
     L.lse2[c] = off;
     off = align_up(off + heads * lse_rows_padded(a->T_max) * sizeof(float));
     L.head_var[c] = off;
@@ -506,6 +518,7 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   const int G = a->H_q / a->H_kv;
   const float scale_log2e = a->scale * kLog2e;
   float4* part = reinterpret_cast<float4*>(w + p.part);
+  float4* part_rest = p.rest_len ? reinterpret_cast<float4*>(w + p.part_rest) : nullptr;
   float* lse2 = reinterpret_cast<float*>(w + p.lse2);
   float* head_var = a->head_var ? a->head_var : reinterpret_cast<float*>(w + p.head_var);
   float* score = a->score_out ? a->score_out : reinterpret_cast<float*>(w + p.score);
@@ -526,6 +539,8 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   ta.split_len = p.split_len;
   ta.n_rgroups = p.n_rgroups;
   ta.part = part;
+  ta.rest_len = p.rest_len;
+  ta.part_rest = part_rest;
   TREVS_TRY(record(a->events, 0, s));
   TREVS_HIP(launch_stats(ta, a->dtype, a->d_head, s));
   TREVS_TRY(record(a->events, 1, s));
@@ -540,6 +555,7 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   ha.n_split = p.n_split;
   ha.text_len = a->text_len;
   ha.lse_rest = a->lse_rest;
+  ha.part_rest = part_rest;
   ha.lse2 = lse2;
   ha.head_var = head_var;
   TREVS_TRY(record(a->events, 2, s));
@@ -643,6 +659,7 @@ trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* a, void* ws, s
   sa.ts = a->ts;
   for (int c = 0; c < 2; ++c) {
     float4* part = reinterpret_cast<float4*>(w + L.part[c]);
+    float4* part_rest = L.sp.rest_len ? reinterpret_cast<float4*>(w + L.part_rest[c]) : nullptr;
     float* lse2 = reinterpret_cast<float*>(w + L.lse2[c]);
     float* head_var = a->head_var[c] ? a->head_var[c] : reinterpret_cast<float*>(w + L.head_var[c]);
     float* profile = a->profile[c] ? a->profile[c] : reinterpret_cast<float*>(w + L.profile[c]);
@@ -662,6 +679,8 @@ trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* a, void* ws, s
     ta.split_len = L.sp.split_len;
     ta.n_rgroups = L.sp.n_rgroups;
     ta.part = part;
+    ta.rest_len = L.sp.rest_len;
+    ta.part_rest = part_rest;
     TREVS_TRY(record(a->events, 6 * c + 0, s));
     TREVS_HIP(launch_stats(ta, a->dtype, a->d_head, s));
     TREVS_TRY(record(a->events, 6 * c + 1, s));
@@ -675,6 +694,7 @@ trevs_status trevs_text_sensitivity(const trevs_sensitivity_args* a, void* ws, s
     ha.n_split = L.sp.n_split;
     ha.text_len = a->text_len[c];
     ha.lse_rest = a->lse_rest[c];
+    ha.part_rest = part_rest;
     ha.lse2 = lse2;
     ha.head_var = head_var;
     TREVS_TRY(record(a->events, 6 * c + 2, s));

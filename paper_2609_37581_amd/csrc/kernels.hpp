@@ -60,6 +60,11 @@ struct StatsArgs {
   int n_split, split_len;    // visual columns per split (multiple of 32)
   int n_rgroups;             // workgroups along the (head-in-group, text row) axis
   float4* part;              // [B,H_q,T_max,n_split]: (max, sum e, sum e^2, -) in log2 units
+  // Causal softmax domain: split s also reduces the non-visual causal keys
+  // [s*rest_len, (s+1)*rest_len) of each text row (key j < P is prefix row j,
+  // j >= P text row j - P, valid for text row q while j - P <= q).
+  int rest_len;              // multiple of 32; 0 for the visual-only domain
+  float4* part_rest;         // [B,H_q,T_max,n_split]: as part, over the non-visual keys
 };
 
 struct HeadArgs {
@@ -67,6 +72,7 @@ struct HeadArgs {
   int B, H_q, T_max, T_pad, K_in, n_split;
   const int32_t* text_len;
   const float* lse_rest;     // [B,H_q,T_max] natural log, or null
+  const float4* part_rest;   // [B,H_q,T_max,n_split] non-visual causal statistics, or null
   float* lse2;               // [B,H_q,T_pad] row log-sum-exp in log2 units (T_pad = T_max rounded up to 32)
   float* head_var;           // [B,H_q] u_h
 };

@@ -25,8 +25,16 @@ constexpr int stats_ring(int vectors_per_tile) { return vectors_per_tile >= 4 ? 
 // are 16 visual columns of its own text row and the softmax statistics stay
 // in-lane.  Workgroups of one (sample, KV head) are numbered consecutively
 // and mapped onto one XCD, so their keys and queries stay in that L2.
+//
+// For the causal softmax domain each workgroup also reduces, into separate
+// (max, sum e), a share of every text row's non-visual causal keys: key index
+// j < P is prefix row j, and j >= P is text row j - P (sequence row
+// j + K_in), valid for text row q while j - P <= q.  Split s takes keys
+// [s*rest_len, (s+1)*rest_len) after its visual keys, in the same tile
+// stream, so the extra work is spread evenly over the grid.  Every row sees
+// at least its own key, so the merged non-visual log-sum-exp is finite.
 // ---------------------------------------------------------------------------
-template <class In, int DH, int NW>
+template <class In, int DH, int NW, bool CAUSAL>
 __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
   constexpr int ROWB = DH * In::kBytes;
   constexpr int HALFB = ROWB / 2;
@@ -58,19 +66,35 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) qf[f][j] = ldg16(qp + f * 64 + j * 16);
   }
+  // visual keys [i_begin, i_end) in nv tiles, then the non-visual causal keys
+  // [j_begin, j_end) in nr tiles
   const int i_begin = split * a.split_len;
   const int i_end = min(a.K_in, i_begin + a.split_len);
+  const int nv = (i_end - i_begin + 31) / 32;
+  const int j_begin = CAUSAL ? min(split * a.rest_len, a.P + a.T_max) : 0;
+  const int j_end = CAUSAL ? min(a.P + a.T_max, j_begin + a.rest_len) : 0;
+  const int n_tiles = nv + (j_end - j_begin + 31) / 32;
+  const int climit = a.P + q;  // last non-visual key index this lane's row attends
   const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) +
-                         ((size_t)b * a.S + a.P) * a.H_kv * ROWB + (size_t)g * ROWB;
+                         (size_t)b * a.S * a.H_kv * ROWB + (size_t)g * ROWB;
   const size_t kstride = (size_t)a.H_kv * ROWB;
-  // one key tile (rows ib..ib+31) into registers; rows past the split re-read
-  // row i_begin (valid, cached)
-  auto load_tile = [&](int ib, u32x4 (&dst)[TVT]) {
+  // tile t into registers: rows past a range (and tiles past the last) re-read
+  // a valid row of the range (cached)
+  auto load_tile = [&](int t, u32x4 (&dst)[TVT]) {
+    const bool vis = !CAUSAL || t < nv || t >= n_tiles;  // uniform
+    const int kb = t < nv ? i_begin + 32 * t : (t < n_tiles ? j_begin + 32 * (t - nv) : i_begin);
 #pragma unroll
     for (int k = 0; k < TVT; ++k) {
       const int v = min(tid + k * NT, TV - 1), row = v / (ROWB / 16), c = v - row * (ROWB / 16);
-      const int i = ib + row;
-      dst[k] = ldg16(kbase + (size_t)(i < i_end ? i : i_begin) * kstride + c * 16);
+      const int i = kb + row;
+      int srow;
+      if (vis) {
+        srow = a.P + (i < i_end ? i : i_begin);
+      } else {
+        const int j = i < j_end ? i : j_begin;
+        srow = j < a.P ? j : j + a.K_in;
+      }
+      dst[k] = ldg16(kbase + (size_t)srow * kstride + c * 16);
     }
   };
   auto store_tile = [&](int buf, const u32x4 (&src)[TVT]) {
@@ -87,10 +111,12 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
   // Online (max, sum e, sum e^2) in log2 units.  The logit scale is positive,
   // so the tile maximum is taken on the raw dot products and scaled once, and
   // each term is exp2(fma(dot, scale, -max)): about four vector operations
-  // and one exp per logit.  Only a split's last tile can hold keys past its
-  // end; it alone takes the masked path.
-  float m = -INFINITY, l = 0.f, l2 = 0.f;
-  auto process = [&](int buf, int ib, auto full) {
+  // and one exp per logit.  Only a split's last visual tile can hold keys
+  // past its end; it alone takes the masked path (so do the non-visual tiles,
+  // whose causal limit differs per row).
+  float m = -INFINITY, l = 0.f, l2 = 0.f;     // visual keys
+  float mr = -INFINITY, lr = 0.f, l2r = 0.f;  // non-visual causal keys
+  auto process = [&](int buf, int kb, int kend, int lim, auto full, float& m_, float& l_, float& l2_) {
     f32x16 acc;
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
@@ -104,15 +130,17 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
     }
     if constexpr (!decltype(full)::value) {
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr)
-        if (ib + mfma_row(rr, half) >= i_end) acc[rr] = -INFINITY;
+      for (int rr = 0; rr < 16; ++rr) {
+        const int i = kb + mfma_row(rr, half);
+        if (i >= kend || i > lim) acc[rr] = -INFINITY;
+      }
     }
     float mx = acc[0];
 #pragma unroll
     for (int rr = 1; rr < 16; ++rr) mx = fmaxf(mx, acc[rr]);
-    const float mn = fmaxf(m, mx * a.scale_log2e);
+    const float mn = fmaxf(m_, mx * a.scale_log2e);
     if (decltype(full)::value || mn > -INFINITY) {
-      const float c = fast_exp2(m - mn);
+      const float c = fast_exp2(m_ - mn);
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
@@ -120,20 +148,19 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
         s1 += e;
         s2 = fmaf(e, e, s2);
       }
-      l = fmaf(l, c, s1);
-      l2 = fmaf(l2, c * c, s2);
-      m = mn;
+      l_ = fmaf(l_, c, s1);
+      l2_ = fmaf(l2_, c * c, s2);
+      m_ = mn;
     }
   };
   // key tiles stream through a ring of RING register buffers (that many
   // tiles in flight from memory) into two alternating LDS buffers; the tiles
-  // past the split are loaded (row i_begin again) but never reduced
+  // past the last are loaded (a valid row again) but never reduced
   constexpr int RING = stats_ring(TVT);
-  const int n_tiles = (i_end - i_begin + 31) / 32;
   const int n_iter = (n_tiles + RING - 1) / RING;
   u32x4 ring[RING][TVT];
 #pragma unroll
-  for (int c = 0; c < RING; ++c) load_tile(i_begin + 32 * c, ring[c]);
+  for (int c = 0; c < RING; ++c) load_tile(c, ring[c]);
   for (int it = 0; it < n_iter; ++it) {
 #pragma unroll
     for (int c = 0; c < RING; ++c) {
@@ -141,32 +168,46 @@ __global__ __launch_bounds__(64 * NW) void t2v_stats_kernel(StatsArgs a) {
       // LDS buffer (t % 2) was last read at tile t - 2, before every wave
       // passed the barrier of tile t - 1
       store_tile(c % 2, ring[c]);
-      load_tile(i_begin + 32 * (t + RING), ring[c]);
+      load_tile(t + RING, ring[c]);
       __syncthreads();
-      const int ib = i_begin + 32 * t;
-      if (ib + 32 <= i_end)
-        process(c % 2, ib, std::true_type{});
-      else if (t < n_tiles)
-        process(c % 2, ib, std::false_type{});
+      if (t < nv) {
+        const int ib = i_begin + 32 * t;
+        if (ib + 32 <= i_end)
+          process(c % 2, ib, i_end, INT_MAX, std::true_type{}, m, l, l2);
+        else
+          process(c % 2, ib, i_end, INT_MAX, std::false_type{}, m, l, l2);
+      } else if (CAUSAL && t < n_tiles) {
+        process(c % 2, j_begin + 32 * (t - nv), j_end, climit, std::false_type{}, mr, lr, l2r);
+      }
     }
   }
-  const float mo = __shfl_xor(m, 32, 64), lo = __shfl_xor(l, 32, 64), l2o = __shfl_xor(l2, 32, 64);
-  const float M = fmaxf(m, mo);
-  float L = 0.f, L2 = 0.f;
-  if (M > -INFINITY) {
-    const float c1 = fast_exp2(m - M), c2 = fast_exp2(mo - M);
-    L = l * c1 + lo * c2;
-    L2 = l2 * c1 * c1 + l2o * c2 * c2;
+  // merge the two half-waves' (max, sum e, sum e^2)
+  auto merge_halves = [&](float m_, float l_, float l2_) {
+    const float mo = __shfl_xor(m_, 32, 64), lo = __shfl_xor(l_, 32, 64), l2o = __shfl_xor(l2_, 32, 64);
+    const float M = fmaxf(m_, mo);
+    float L = 0.f, L2 = 0.f;
+    if (M > -INFINITY) {
+      const float c1 = fast_exp2(m_ - M), c2 = fast_exp2(mo - M);
+      L = l_ * c1 + lo * c2;
+      L2 = l2_ * c1 * c1 + l2o * c2 * c2;
+    }
+    return make_float4(M, L, L2, 0.f);
+  };
+  const size_t slot = (((size_t)b * a.H_q + h) * a.T_max + q) * a.n_split + split;
+  const float4 vs = merge_halves(m, l, l2);
+  if (half == 0 && rvalid) a.part[slot] = vs;
+  if constexpr (CAUSAL) {
+    const float4 rs = merge_halves(mr, lr, l2r);
+    if (half == 0 && rvalid) a.part_rest[slot] = rs;
   }
-  if (half == 0 && rvalid)
-    a.part[(((size_t)b * a.H_q + h) * a.T_max + q) * a.n_split + split] = make_float4(M, L, L2, 0.f);
 }
 
 // ---------------------------------------------------------------------------
 // Head pass, one workgroup per (head, sample).  Merges the split statistics
 // of every text row into its log-sum-exp (optionally joined with the row's
-// non-visual log-sum-exp) and the population variance of the row's visual
-// attention, then averages over the valid text rows: u_h of Eq. (8).
+// non-visual log-sum-exp, given by the caller or merged from the causal rest
+// statistics) and the population variance of the row's visual attention,
+// then averages over the valid text rows: u_h of Eq. (8).
 // ---------------------------------------------------------------------------
 constexpr int kHeadThreads = 128;
 
@@ -192,8 +233,22 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
       m = mn;
     }
     float lse2 = m + log2f(l);
-    if (a.lse_rest) {
-      const float r2 = a.lse_rest[row] * kLog2e;
+    if (a.lse_rest || a.part_rest) {
+      float r2;
+      if (a.part_rest) {
+        const float4* pr = a.part_rest + row * a.n_split;
+        float mr = -INFINITY, lr = 0.f;
+        for (int s = 0; s < a.n_split; ++s) {
+          const float4 p = pr[s];
+          const float mn = fmaxf(mr, p.x);
+          if (mn == -INFINITY) continue;
+          lr = lr * fast_exp2(mr - mn) + p.y * fast_exp2(p.x - mn);
+          mr = mn;
+        }
+        r2 = mr + log2f(lr);
+      } else {
+        r2 = a.lse_rest[row] * kLog2e;
+      }
       const float mx = fmaxf(lse2, r2);
       lse2 = mx + log2f(fast_exp2(lse2 - mx) + fast_exp2(r2 - mx));
     }
@@ -411,15 +466,23 @@ int stats_waves(int G, int T_max) {
   return nrb >= 8 ? 8 : (nrb >= 4 ? 4 : (nrb >= 2 ? 2 : 1));
 }
 
-template <class In, int DH>
-static void launch_stats_t(const StatsArgs& a, hipStream_t s) {
+template <class In, int DH, bool CAUSAL>
+static void launch_stats_c(const StatsArgs& a, hipStream_t s) {
   const dim3 grid(a.n_split * a.n_rgroups * a.H_kv * a.B);
   switch (stats_waves(a.G, a.T_max)) {
-    case 8: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 8>), grid, dim3(512), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 4>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 2>), grid, dim3(128), 0, s, a); break;
-    default: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 1>), grid, dim3(64), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 8, CAUSAL>), grid, dim3(512), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 4, CAUSAL>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 2, CAUSAL>), grid, dim3(128), 0, s, a); break;
+    default: hipLaunchKernelGGL((t2v_stats_kernel<In, DH, 1, CAUSAL>), grid, dim3(64), 0, s, a); break;
   }
+}
+
+template <class In, int DH>
+static void launch_stats_t(const StatsArgs& a, hipStream_t s) {
+  if (a.rest_len > 0)
+    launch_stats_c<In, DH, true>(a, s);
+  else
+    launch_stats_c<In, DH, false>(a, s);
 }
 
 template <class In>

@@ -24,6 +24,8 @@ INLLM_KERNELS = ("t2v_stats", "head_var", "token_score", "topk", "compaction")
 SENSITIVITY_KERNELS = ("t2v_stats.0", "head_var.0", "profile.0", "t2v_stats.1", "head_var.1",
                        "profile.1", "sensitivity")
 
+SOFTMAX = {"visual": 0, "causal": 1}  # trevs_softmax
+
 _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "workspace", 4: "hip error"}
 
 
@@ -62,7 +64,7 @@ class InllmArgs(ctypes.Structure):
                 ("lse_rest", c_void_p), ("kept_idx", c_void_p), ("hidden_out", c_void_p),
                 ("k_out", c_void_p), ("v_out", c_void_p), ("pos_out", c_void_p),
                 ("head_sel", c_void_p), ("head_var", c_void_p), ("score_out", c_void_p),
-                ("events", c_void_p)]
+                ("events", c_void_p), ("softmax", c_int32)]
 
 
 class SensitivityArgs(ctypes.Structure):
@@ -71,7 +73,7 @@ class SensitivityArgs(ctypes.Structure):
                 ("d_head", c_int32), ("scale", c_float), ("dtype", c_int32),
                 ("q", c_void_p * 2), ("k", c_void_p * 2), ("text_len", c_void_p * 2),
                 ("lse_rest", c_void_p * 2), ("ts", c_void_p), ("profile", c_void_p * 2),
-                ("head_var", c_void_p * 2), ("events", c_void_p)]
+                ("head_var", c_void_p * 2), ("events", c_void_p), ("softmax", c_int32)]
 
 
 _lib = None
@@ -251,7 +253,7 @@ class Inllm:
     """Stage 2 with outputs and workspace allocated once; call() enqueues it."""
 
     def __init__(self, q, k, v, hidden, pos, text_len=None, *, P, K_in, n_keep_heads, k_keep,
-                 scale=None, lse_rest=None, want_scores=False):
+                 scale=None, lse_rest=None, want_scores=False, softmax="visual"):
         dev = hidden.device
         _check(hidden, "hidden", dev, 3)
         dt = hidden.dtype
@@ -298,6 +300,7 @@ class Inllm:
         a.dtype = _dtype_code(hidden)
         a.q, a.k, a.v, a.hidden, a.pos = _ptr(q), _ptr(k), _ptr(v), _ptr(hidden), _ptr(pos)
         a.text_len, a.lse_rest = _ptr(text_len), _ptr(lse_rest)
+        a.softmax = SOFTMAX[softmax]
         a.kept_idx, a.hidden_out = _ptr(self.kept_idx), _ptr(self.hidden_out)
         a.k_out, a.v_out, a.pos_out = _ptr(self.k_out), _ptr(self.v_out), _ptr(self.pos_out)
         a.head_sel, a.head_var, a.score_out = _ptr(self.head_sel), _ptr(self.head_var), _ptr(self.score)
@@ -349,7 +352,7 @@ class TextSensitivity:
     variances [B,H_q]; allocated once, call() enqueues the computation."""
 
     def __init__(self, q, k, q2, k2, text_len=None, text_len2=None, *, P, K_in, scale=None,
-                 lse_rest=None, lse_rest2=None):
+                 lse_rest=None, lse_rest2=None, softmax="visual"):
         dev = q.device
         dt = q.dtype
         for t, name in ((q, "q"), (k, "k"), (q2, "q2"), (k2, "k2")):
@@ -382,6 +385,7 @@ class TextSensitivity:
         a.q[0], a.q[1], a.k[0], a.k[1] = _ptr(q), _ptr(q2), _ptr(k), _ptr(k2)
         a.text_len[0], a.text_len[1] = _ptr(text_len), _ptr(text_len2)
         a.lse_rest[0], a.lse_rest[1] = _ptr(lse_rest), _ptr(lse_rest2)
+        a.softmax = SOFTMAX[softmax]
         a.ts = _ptr(self.ts)
         a.profile[0], a.profile[1] = _ptr(self.profile[0]), _ptr(self.profile[1])
         a.head_var[0], a.head_var[1] = _ptr(self.head_var[0]), _ptr(self.head_var[1])

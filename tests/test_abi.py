@@ -41,8 +41,8 @@ def test_every_declared_symbol_is_exported():
 def test_struct_mirror_sizes():
     L = trevs.lib()
     assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 168
-    assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 192
-    assert L.trevs_sensitivity_args_size() == ctypes.sizeof(trevs.SensitivityArgs) == 160
+    assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 200
+    assert L.trevs_sensitivity_args_size() == ctypes.sizeof(trevs.SensitivityArgs) == 168
 
 
 def test_status_strings_and_keep_count():
@@ -91,6 +91,9 @@ def test_workspace_size_is_positive_for_valid_args():
     plain = L.trevs_prellm_workspace_size(ctypes.byref(_prellm()))
     assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm(k_div=48))) >= plain + 2 * 576 * 576 * 4
     assert L.trevs_inllm_workspace_size(ctypes.byref(_inllm())) > 0
+    # the causal softmax adds the non-visual statistics of every text row
+    vis = L.trevs_inllm_workspace_size(ctypes.byref(_inllm()))
+    assert L.trevs_inllm_workspace_size(ctypes.byref(_inllm(softmax=1))) >= vis + 2 * 32 * 32 * 16
 
 
 @pytest.mark.parametrize("bad,code", [
@@ -126,6 +129,8 @@ def test_prellm_workspace_errors():
     (dict(hidden_out=None), 1), (dict(d_head=96), 2), (dict(D=4095), 1), (dict(pos=(1 << 40) + 4), 1),
     (dict(K_in=40000, S=40100, T_max=10), 2),
     (dict(k_out=(1 << 40) + (1 << 32) + 1024), 1),  # overlaps k
+    (dict(softmax=2), 1), (dict(softmax=-1), 1),
+    (dict(softmax=1, lse_rest=(1 << 40) + (11 << 32)), 1),  # lse_rest is for the visual domain
 ])
 def test_inllm_rejects_before_launch(bad, code):
     L = trevs.lib()
@@ -175,6 +180,7 @@ def test_sensitivity_workspace_covers_both_questions():
     (dict(ts=(1 << 40) + (2 << 32) + 64), 1),  # overlaps the keys
     (dict(profile=(1, (1 << 40) + 1024)), 1),  # overlaps question 0's queries
     (dict(head_var=(0, (1 << 40) + (5 << 32) + 2)), 1),  # misaligned
+    (dict(softmax=5), 1), (dict(softmax=1, lse_rest=(1, (1 << 40) + (6 << 32))), 1),
 ])
 def test_sensitivity_rejects_before_launch(bad, code):
     L = trevs.lib()

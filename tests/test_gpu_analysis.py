@@ -16,7 +16,7 @@ from synthetic import WORKLOADS, sensitivity_inputs, stage1_inputs
 pytestmark = pytest.mark.gpu
 
 
-def run_sensitivity(inp, w, use_lse_rest=False, shared_k=True):
+def run_sensitivity(inp, w, use_lse_rest=False, shared_k=True, softmax="visual"):
     q0 = dev_tensor(inp["q0"], w.dtype)
     q1 = dev_tensor(inp["q1"], w.dtype)
     k0 = dev_tensor(inp["k"], w.dtype)
@@ -26,19 +26,20 @@ def run_sensitivity(inp, w, use_lse_rest=False, shared_k=True):
     lr0 = torch.from_numpy(inp["lse_rest0"]).cuda() if use_lse_rest else None
     lr1 = torch.from_numpy(inp["lse_rest1"]).cuda() if use_lse_rest else None
     ts, prof, hv = trevs.text_sensitivity(q0, k0, q1, k1, tl0, tl1, P=w.P, K_in=w.K1,
-                                          lse_rest=lr0, lse_rest2=lr1)
+                                          lse_rest=lr0, lse_rest2=lr1, softmax=softmax)
     torch.cuda.synchronize()
     return dict(ts=ts.cpu().numpy(), profile0=prof[0].cpu().numpy(),
                 profile1=prof[1].cpu().numpy(), head_var0=hv[0].cpu().numpy(),
                 head_var1=hv[1].cpu().numpy())
 
 
-def oracle_sensitivity(inp, w, use_lse_rest=False):
+def oracle_sensitivity(inp, w, use_lse_rest=False, softmax="visual"):
     return oracle.sensitivity(inp["q0"], inp["k"], inp["q1"], inp["k"], inp["text_len0"],
                               inp["text_len1"], w.dtype, P=w.P, K1=w.K1,
                               scale=1.0 / math.sqrt(w.d_h),
                               lse_rest1=inp["lse_rest0"] if use_lse_rest else None,
-                              lse_rest2=inp["lse_rest1"] if use_lse_rest else None)
+                              lse_rest2=inp["lse_rest1"] if use_lse_rest else None,
+                              softmax=softmax)
 
 
 # TS lies in [0, 1]; besides the relative bar it gets an absolute floor of
@@ -86,6 +87,20 @@ def test_text_sensitivity_full_row_softmax():
     inp = sensitivity_inputs(w, with_lse_rest=True)
     g = run_sensitivity(inp, w, use_lse_rest=True)
     check_sensitivity(g, oracle_sensitivity(inp, w, use_lse_rest=True))
+
+
+@pytest.mark.parametrize("name", ["llava15-b4-bf16-ragged-text", "ragged-bf16-dh64",
+                                  "qwen25vl-b1-bf16-gqa"])
+def test_text_sensitivity_causal_softmax(name):
+    """Eq. (1) on the visual columns of each text row's whole causal
+    attention row, computed by the library from q and k."""
+    w = SENS_CASES[name]
+    print(f"[sensitivity] causal {name}", flush=True)
+    inp = sensitivity_inputs(w)
+    g = run_sensitivity(inp, w, softmax="causal")
+    check_sensitivity(g, oracle_sensitivity(inp, w, softmax="causal"))
+    # a causal profile carries only the visual share of each row
+    assert (g["profile0"].sum(-1) < 1).all()
 
 
 def test_text_sensitivity_same_question_is_zero():

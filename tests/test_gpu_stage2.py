@@ -15,7 +15,7 @@ from synthetic import WORKLOADS, stage2_inputs
 pytestmark = pytest.mark.gpu
 
 
-def run_gpu(inp, w, n_keep=None, k_keep=None, use_lse_rest=False):
+def run_gpu(inp, w, n_keep=None, k_keep=None, use_lse_rest=False, softmax="visual"):
     q = dev_tensor(inp["q"], w.dtype)
     k = dev_tensor(inp["k"], w.dtype)
     v = dev_tensor(inp["v"], w.dtype)
@@ -24,7 +24,7 @@ def run_gpu(inp, w, n_keep=None, k_keep=None, use_lse_rest=False):
     tl = torch.from_numpy(inp["text_len"]).cuda()
     lr = torch.from_numpy(inp["lse_rest"]).cuda() if use_lse_rest else None
     call = trevs.Inllm(q, k, v, hid, pos, tl, P=w.P, K_in=w.K1, n_keep_heads=n_keep or w.n_keep,
-                       k_keep=k_keep or w.K2, lse_rest=lr, want_scores=True)
+                       k_keep=k_keep or w.K2, lse_rest=lr, want_scores=True, softmax=softmax)
     call()
     torch.cuda.synchronize()
     return dict(kept_idx=call.kept_idx.cpu().numpy(), hidden_out=host_bits(call.hidden_out),
@@ -33,23 +33,24 @@ def run_gpu(inp, w, n_keep=None, k_keep=None, use_lse_rest=False):
                 head_var=call.head_var.cpu().numpy(), score=call.score.cpu().numpy())
 
 
-def run_oracle(inp, w, n_keep, k_keep, use_lse_rest=False, heads=None):
+def run_oracle(inp, w, n_keep, k_keep, use_lse_rest=False, heads=None, softmax="visual"):
     return oracle.inllm(inp["q"], inp["k"], inp["v"], inp["hidden"], inp["pos"], inp["text_len"],
                         w.dtype, P=w.P, K1=w.K1, n_keep=n_keep, k_keep=k_keep,
                         scale=1.0 / math.sqrt(w.d_h),
-                        lse_rest=inp["lse_rest"] if use_lse_rest else None, heads=heads)
+                        lse_rest=inp["lse_rest"] if use_lse_rest else None, heads=heads,
+                        softmax=softmax)
 
 
-def check(inp, w, g, n_keep=None, k_keep=None, use_lse_rest=False):
+def check(inp, w, g, n_keep=None, k_keep=None, use_lse_rest=False, softmax="visual"):
     n_keep = n_keep or w.n_keep
     k_keep = k_keep or w.K2
-    o = run_oracle(inp, w, n_keep, k_keep, use_lse_rest)
+    o = run_oracle(inp, w, n_keep, k_keep, use_lse_rest, softmax=softmax)
     assert_scores_close(g["head_var"], o["head_var"], "u_h")
     assert_kept_band(g["head_sel"], o["head_var"], n_keep, "H*")
     assert_kept_exact_on_own_scores(g["head_sel"], g["head_var"], n_keep, "H*")
     if not np.array_equal(g["head_sel"], o["head_sel"]):
         # heads tied within tolerance: score the oracle with the kernel's head set
-        o = run_oracle(inp, w, n_keep, k_keep, use_lse_rest, heads=g["head_sel"])
+        o = run_oracle(inp, w, n_keep, k_keep, use_lse_rest, heads=g["head_sel"], softmax=softmax)
     assert_scores_close(g["score"], o["score"], "p")
     assert_kept_band(g["kept_idx"], o["score"], k_keep, "kept")
     assert_kept_exact_on_own_scores(g["kept_idx"], g["score"], k_keep, "kept")
@@ -99,6 +100,37 @@ def test_stage2_lse_rest_full_row_softmax():
     check(inp, w, g, use_lse_rest=True)
 
 
+CAUSAL_CASES = {
+    "llava15-b3-bf16-ragged-text": WORKLOADS["llava15-b64-bf16"].with_(B=3),
+    "llava15-b1-f32": WORKLOADS["llava15-b1-f32"],
+    # a prefix longer than a key split (P + T_max = 195 > 128: two splits of
+    # the non-visual keys), ragged rows, GQA 12/3, d_head 64
+    "long-prefix-gqa-dh64": WORKLOADS["llava15-b64-bf16"].with_(
+        B=2, K1=77, K2=20, M_max=45, text_len=("uniform", 1, 45), P=150, H_q=12, H_kv=3,
+        d_h=64, D=200, n_keep=5, N=400, grid=20),
+    # no prefix: text row 0 sees only its own non-visual key
+    "no-prefix-mqa-dh256": WORKLOADS["llava15-b64-bf16"].with_(
+        B=2, K1=130, K2=30, M_max=33, text_len=("uniform", 20, 33), P=0, H_q=8, H_kv=1,
+        d_h=256, D=64, n_keep=3),
+    "one-text-row-f32-dh256": WORKLOADS["llava15-b1-f32"].with_(
+        B=2, K1=50, K2=9, M_max=1, H_q=4, H_kv=2, d_h=256, D=48, n_keep=2),
+}
+
+
+@pytest.mark.parametrize("name", list(CAUSAL_CASES))
+def test_stage2_causal_softmax(name):
+    """The softmax over each text row's whole causal row, computed by the
+    library from q and k (prefix, visual and text keys up to the row)."""
+    w = CAUSAL_CASES[name]
+    print(f"[stage2] causal {name}: B={w.B} P={w.P} K1={w.K1} T={w.T_max} H={w.H_q}/{w.H_kv} "
+          f"dh={w.d_h} {w.dtype}", flush=True)
+    inp = stage2_inputs(w)
+    g = run_gpu(inp, w, softmax="causal")
+    o = check(inp, w, g, softmax="causal")
+    # the visual block takes only part of each causal row
+    assert (o["head_var"] < run_oracle(inp, w, w.n_keep, w.K2)["head_var"]).all()
+
+
 @pytest.mark.parametrize("n_keep,k_keep", [(32, 64), (1, 64), (16, 192), (16, 1), (4, 11)])
 def test_stage2_keep_extremes(n_keep, k_keep):
     w = WORKLOADS["llava15-b64-bf16"].with_(B=2)
@@ -128,6 +160,14 @@ def test_stage2_full_size_qwen(qwen_full):
     # planted structure: the sensitive heads have the highest variance
     for b in range(w.B):
         assert np.isin(inp["relevant"][b], g["kept_idx"][b]).mean() > 0.8
+
+
+def test_stage2_full_size_qwen_causal(qwen_full):
+    """The benchmarked shape with the causal softmax domain."""
+    w, inp = qwen_full
+    print("[stage2] full-size qwen, causal softmax", flush=True)
+    g = run_gpu(inp, w, softmax="causal")
+    check(inp, w, g, softmax="causal")
 
 
 def test_stage2_run_to_run_bit_identical(qwen_full):
