@@ -1,5 +1,6 @@
 // Stage 2 (in-LLM) kernels: text->vision attention statistics, head variance
 // and high-variance head set, and the token score (Sec. 4.2, Eq. (8)-(9)).
+#include <algorithm>
 #include <type_traits>
 
 #include "common.hpp"
@@ -271,17 +272,19 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
 // ---------------------------------------------------------------------------
 // Token score.  A workgroup owns V = 32*VB visual tokens of one sample (tiles
 // of one sample are numbered consecutively and mapped onto one XCD, so the
-// sample's queries stay in that L2).  It first ranks the heads of its sample
-// by (u desc, h asc) and keeps the first n_keep: the high-variance set H*,
-// ascending (the sample's first tile also stores it).  Wave w takes the
-// 32-row text blocks w, w+QW, ...: for each selected head the key rows of the
-// tile (the head's KV group) sit in LDS (two buffers alternate, the next
-// head's tile is staged while the current one is used), the wave's Q rows and
-// row log-sum-exps are prefetched into registers one head ahead, the logits
-// are recomputed on the matrix cores (operand A = text rows, operand B = key
-// rows) and turned into attention, and the attention is summed over heads
-// in-lane.  Then max over the valid text rows, across waves via LDS, and
-// divide by |H*| (Eq. (9)).
+// sample's queries and keys stay in that L2).  It first ranks the heads of
+// its sample by (u desc, h asc) and keeps the first n_keep: the
+// high-variance set H*, ascending (the sample's first tile also stores it).
+// Wave w owns the 32 text rows of block pass*QW + w and all V keys.  For each
+// selected head the pass's Q rows (QW*32 of them) and their row log-sum-exps
+// are staged in LDS with coalesced 16-byte loads (a 32-row MFMA operand read
+// straight from memory would touch 32 rows per instruction), one head ahead.
+// H* is ascending, so its heads of one KV group are consecutive: the key tile
+// of a group is staged in LDS once and serves every selected head of the
+// group (the next group's tile waits in registers).  The logits are
+// recomputed on the matrix cores (operand A = text rows, operand B = key
+// rows), turned into attention and summed over heads in-lane.  Then max over
+// the valid text rows, across waves via LDS, and divide by |H*| (Eq. (9)).
 // ---------------------------------------------------------------------------
 constexpr int kMaxHeads = 256;
 
@@ -296,14 +299,18 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
   constexpr int ROWB = DH * In::kBytes;
   constexpr int HALFB = ROWB / 2;
   constexpr int NF = HALFB / 64;
-  constexpr int NT = 64 * QW;
   constexpr int VB = ScoreTile<ROWB>::VB;
   constexpr int V = ScoreTile<ROWB>::V;
+  constexpr int NT = 64 * QW;
   constexpr int LROW = ROWB + 16;
   constexpr int CPR = ROWB / 16;
-  constexpr int TV = V * CPR;
-  constexpr int TVT = (TV + NT - 1) / NT;
+  constexpr int QR = 32 * QW;                  // text rows of a pass
+  constexpr int KVT = V * CPR / NT;            // 16-byte vectors per thread: key tile
+  constexpr int QVT = QR * CPR / NT;           // ... and Q rows
+  static_assert(KVT * NT == V * CPR && QVT * NT == QR * CPR, "stage split");
   __shared__ __attribute__((aligned(16))) uint8_t klds[2][V * LROW];
+  __shared__ __attribute__((aligned(16))) uint8_t qlds[2][QR * LROW];
+  __shared__ __attribute__((aligned(16))) float llds[2][QR];
   __shared__ float pmax[QW][V];
   __shared__ float u_lds[kMaxHeads];
   __shared__ int sel_lds[kMaxHeads];
@@ -314,29 +321,38 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
   const int b = lin / a.n_vtiles, i0 = (lin - b * a.n_vtiles) * V;
   const int Hq = a.H_q, nk = a.n_keep;
 
-  // ---- high-variance head set H*
+  // ---- high-variance head set H*: the rank of head h under (u desc, h asc)
+  // counts the heads before it, 64 comparisons per ballot (wave w ranks heads
+  // w, w + QW, ...); wave 0 then writes the selected heads in ascending order
   for (int h = tid; h < Hq; h += NT) {
     u_lds[h] = a.head_var[(size_t)b * Hq + h];
     heads[h] = 0;
   }
   __syncthreads();
-  for (int h = tid; h < Hq; h += NT) {
+  for (int h = wave; h < Hq; h += QW) {
     const float u = u_lds[h];
     int rank = 0;
-    for (int h2 = 0; h2 < Hq; ++h2) {
-      const float u2 = u_lds[h2];
-      rank += (u2 > u || (u2 == u && h2 < h)) ? 1 : 0;
+    for (int c0 = 0; c0 < Hq; c0 += 64) {
+      const int h2 = c0 + lane;
+      const float u2 = h2 < Hq ? u_lds[h2] : 0.f;
+      rank += (int)__popcll(__ballot(h2 < Hq && (u2 > u || (u2 == u && h2 < h))));
     }
-    sel_lds[h] = rank < nk;
+    if (lane == 0) sel_lds[h] = rank < nk;
   }
   __syncthreads();
-  for (int h = tid; h < Hq; h += NT) {
-    if (!sel_lds[h]) continue;
-    int pos = 0;
-    for (int h2 = 0; h2 < h; ++h2) pos += sel_lds[h2];
-    if (pos < nk) {  // ranks are distinct for finite u
-      heads[pos] = h;
-      if (i0 == 0 && a.head_sel) a.head_sel[(size_t)b * nk + pos] = h;
+  if (wave == 0) {
+    int base = 0;
+    for (int c0 = 0; c0 < Hq; c0 += 64) {
+      const int h = c0 + lane;
+      const bool sel = h < Hq && sel_lds[h];
+      const unsigned long long bal = __ballot(sel);
+      const int pos = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+      if (sel && pos < nk) {  // ranks are distinct for finite u
+        heads[pos] = h;
+        if (i0 == 0 && a.head_sel) a.head_sel[(size_t)b * nk + pos] = h;
+      }
+      base += (int)__popcll(bal);
     }
   }
   __syncthreads();
@@ -346,23 +362,29 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
   const size_t seq0 = (size_t)b * a.S;
   const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) + (seq0 + a.P) * a.H_kv * ROWB;
   const size_t kstride = (size_t)a.H_kv * ROWB;
+  const uint8_t* qtext = reinterpret_cast<const uint8_t*>(a.q) + (seq0 + a.P + a.K_in) * a.H_q * ROWB;
+  const size_t qstride = (size_t)a.H_q * ROWB;
+  // first head index after hi that belongs to another KV group
+  auto next_group = [&](int hi) {
+    const int g = head_at(hi) / a.G;
+    int j = hi + 1;
+    while (j < nk && head_at(j) / a.G == g) ++j;
+    return j;
+  };
   // key rows i0..i0+V-1 of KV group g (rows past K_in re-read the last row)
-  auto load_tile = [&](int g, u32x4 (&dst)[TVT]) {
+  auto load_tile = [&](int g, u32x4 (&dst)[KVT]) {
 #pragma unroll
-    for (int k = 0; k < TVT; ++k) {
-      const int v = min(tid + k * NT, TV - 1), row = v / CPR, c = v - row * CPR;
+    for (int k = 0; k < KVT; ++k) {
+      const int v = tid + k * NT, row = v / CPR, c = v - row * CPR;
       const int i = min(i0 + row, a.K_in - 1);
       dst[k] = ldg16(kbase + (size_t)i * kstride + (size_t)g * ROWB + c * 16);
     }
   };
-  auto store_tile = [&](int buf, const u32x4 (&src)[TVT]) {
+  auto store_tile = [&](int buf, const u32x4 (&src)[KVT]) {
 #pragma unroll
-    for (int k = 0; k < TVT; ++k) {
-      const int v = tid + k * NT;
-      if (v < TV) {
-        const int row = v / CPR, c = v - row * CPR;
-        *reinterpret_cast<u32x4*>(&klds[buf][row * LROW + c * 16]) = src[k];
-      }
+    for (int k = 0; k < KVT; ++k) {
+      const int v = tid + k * NT, row = v / CPR, c = v - row * CPR;
+      *reinterpret_cast<u32x4*>(&klds[buf][row * LROW + c * 16]) = src[k];
     }
   };
 
@@ -372,32 +394,47 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
   const int n_qblk = (Tb + 31) / 32;
   const int n_pass = (n_qblk + QW - 1) / QW;  // uniform over the workgroup (barriers below)
   for (int pass = 0; pass < n_pass; ++pass) {
-    const int qb = pass * QW + wave;
-    const int qrow = min(qb * 32 + col, a.T_max - 1);
-    const uint8_t* qbase = reinterpret_cast<const uint8_t*>(a.q) +
-                           ((seq0 + a.P + a.K_in + qrow) * a.H_q) * ROWB + half * HALFB;
-    // rows of the lse workspace are padded to a multiple of 32, so the float4
-    // reads of a 32-row block stay inside it
-    const int lq = min(qb, (a.T_max - 1) / 32) * 32 + 4 * half;
-    auto load_q = [&](int hi, u32x4 (&qf)[NF][4], float4 (&lse)[4]) {
+    const int r0 = pass * QR;
+    // text rows r0..r0+QR-1 of head index hi (rows past T_max re-read the
+    // last row) and their log-sum-exps (float4s, every thread one; duplicates
+    // store the same values; the row is padded to a multiple of 32)
+    auto load_q = [&](int hi, u32x4 (&dst)[QVT], float4& ldst) {
       const int h = head_at(hi);
 #pragma unroll
-      for (int f = 0; f < NF; ++f)
+      for (int k = 0; k < QVT; ++k) {
+        const int v = tid + k * NT, row = v / CPR, c = v - row * CPR;
+        const int t = min(r0 + row, a.T_max - 1);
+        dst[k] = ldg16(qtext + (size_t)t * qstride + (size_t)h * ROWB + c * 16);
+      }
+      ldst = *reinterpret_cast<const float4*>(a.lse2 + ((size_t)b * a.H_q + h) * a.T_pad +
+                                              min(r0 + 4 * (tid % (QR / 4)), a.T_pad - 4));
+    };
+    auto store_q = [&](int buf, const u32x4 (&src)[QVT], float4 l) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) qf[f][j] = ldg16(qbase + (size_t)h * ROWB + f * 64 + j * 16);
-      const float* lrow = a.lse2 + ((size_t)b * a.H_q + h) * a.T_pad + lq;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) lse[j] = *reinterpret_cast<const float4*>(lrow + 8 * j);
+      for (int k = 0; k < QVT; ++k) {
+        const int v = tid + k * NT, row = v / CPR, c = v - row * CPR;
+        *reinterpret_cast<u32x4*>(&qlds[buf][row * LROW + c * 16]) = src[k];
+      }
+      *reinterpret_cast<float4*>(&llds[buf][4 * (tid % (QR / 4))]) = l;
     };
     float accs[VB][16];
 #pragma unroll
     for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) accs[vb][rr] = 0.f;
-    auto process = [&](const u32x4 (&qf)[NF][4], const float4 (&lse)[4], int buf) {
+    auto process = [&](int qbuf, int kbuf) {
+      const uint8_t* qp = &qlds[qbuf][(wave * 32 + col) * LROW + half * HALFB];
+      u32x4 qf[NF][4];
+#pragma unroll
+      for (int f = 0; f < NF; ++f)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) qf[f][j] = *reinterpret_cast<const u32x4*>(qp + f * 64 + j * 16);
+      float4 lse[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) lse[j] = *reinterpret_cast<const float4*>(&llds[qbuf][wave * 32 + 8 * j + 4 * half]);
 #pragma unroll
       for (int vb = 0; vb < VB; ++vb) {
-        const uint8_t* p = &klds[buf][(vb * 32 + col) * LROW + half * HALFB];
+        const uint8_t* p = &klds[kbuf][(vb * 32 + col) * LROW + half * HALFB];
         f32x16 acc;
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
@@ -417,31 +454,44 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
         }
       }
     };
-    u32x4 kst[TVT], qA[NF][4], qB[NF][4];
-    float4 lA[4], lB[4];
+    // group runs of H*: the first run's key tile goes to buffer 0, the next
+    // run's tile waits in registers until its run starts
+    u32x4 kst[KVT];
     load_tile(head_at(0) / a.G, kst);
     store_tile(0, kst);
-    __syncthreads();
-    load_tile(head_at(1) / a.G, kst);
-    load_q(0, qA, lA);
-    load_q(1, qB, lB);
+    int he = next_group(0);
+    if (he < nk) load_tile(head_at(he) / a.G, kst);
+    int kbuf = 0;
+    u32x4 qr[QVT];
+    float4 lr;
+    load_q(0, qr, lr);
     for (int hi = 0; hi < nk; hi += 2) {
-      process(qA, lA, 0);
-      store_tile(1, kst);
-      __syncthreads();
-      load_tile(head_at(hi + 2) / a.G, kst);
-      load_q(hi + 2, qA, lA);
-      if (hi + 1 < nk) process(qB, lB, 1);
-      store_tile(0, kst);
-      __syncthreads();
-      load_tile(head_at(hi + 3) / a.G, kst);
-      load_q(hi + 3, qB, lB);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int h = hi + c;
+        if (h < nk) {  // uniform over the workgroup
+          // Q buffer c was last read at head h - 2, before every wave passed
+          // the barrier of head h - 1; a new group's key buffer was last
+          // read two groups back, before the barrier of this group's start
+          if (h > 0 && h == he) {
+            kbuf ^= 1;
+            store_tile(kbuf, kst);
+            he = next_group(h);
+            if (he < nk) load_tile(head_at(he) / a.G, kst);
+          }
+          store_q(c, qr, lr);
+          __syncthreads();
+          load_q(h + 1, qr, lr);
+          process(c, kbuf);
+        }
+      }
     }
 #pragma unroll
     for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr)
-        if (qb * 32 + mfma_row(rr, half) < Tb) pm[vb] = fmaxf(pm[vb], accs[vb][rr]);
+        if (r0 + wave * 32 + mfma_row(rr, half) < Tb) pm[vb] = fmaxf(pm[vb], accs[vb][rr]);
+    __syncthreads();  // the next pass restages every buffer
   }
   // operand A = text rows: a lane holds text rows of visual column (vb*32 + col)
 #pragma unroll
@@ -508,9 +558,12 @@ hipError_t launch_heads(const HeadArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-int score_qblocks(int T_max) {
+// 32-row text blocks per pass of the token-score workgroup (its waves); the
+// Q rows of a pass are double-buffered in LDS, so long rows take fewer.
+int score_qblocks(int T_max, int row_bytes) {
   const int qb = (T_max + 31) / 32;
-  return qb >= 4 ? 4 : (qb >= 2 ? 2 : 1);
+  const int cap = row_bytes <= 256 ? 4 : (row_bytes <= 512 ? 2 : 1);
+  return std::min(cap, qb >= 4 ? 4 : (qb >= 2 ? 2 : 1));
 }
 
 int score_tile_tokens(int dtype, int dh) {
@@ -521,11 +574,21 @@ int score_tile_tokens(int dtype, int dh) {
 template <class In, int DH>
 static void launch_score_t(const ScoreArgs& a, hipStream_t s) {
   const dim3 grid(a.B * a.n_vtiles);
-  switch (score_qblocks(a.T_max)) {
-    case 4: hipLaunchKernelGGL((t2v_score_kernel<In, DH, 4>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((t2v_score_kernel<In, DH, 2>), grid, dim3(128), 0, s, a); break;
-    default: hipLaunchKernelGGL((t2v_score_kernel<In, DH, 1>), grid, dim3(64), 0, s, a); break;
+  constexpr int ROWB = DH * In::kBytes;
+  const int qw = score_qblocks(a.T_max, ROWB);
+  if constexpr (ROWB <= 256) {
+    if (qw == 4) {
+      hipLaunchKernelGGL((t2v_score_kernel<In, DH, 4>), grid, dim3(256), 0, s, a);
+      return;
+    }
   }
+  if constexpr (ROWB <= 512) {
+    if (qw == 2) {
+      hipLaunchKernelGGL((t2v_score_kernel<In, DH, 2>), grid, dim3(128), 0, s, a);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((t2v_score_kernel<In, DH, 1>), grid, dim3(64), 0, s, a);
 }
 
 template <class In>
