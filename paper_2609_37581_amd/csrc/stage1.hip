@@ -532,16 +532,22 @@ __global__ __launch_bounds__(kSelThreads) void fuse_topk_kernel(SelArgs a) {
   const float med_v = a.stats[4 * b + 0], mad_v = a.stats[4 * b + 1];
   const float med_t = a.stats[4 * b + 2], mad_t = a.stats[4 * b + 3];
   if (a.norm_stats && tid < 4) a.norm_stats[4 * b + tid] = a.stats[4 * b + tid];
-  const float den_v = mad_v + a.eps, den_t = mad_t + a.eps;
+  // one workgroup holds a whole sample, so the per-token arithmetic is kept
+  // to multiplies: the branch weight, 1/(MAD + eps) and 1/tau are folded into
+  // one factor per branch, and the square root is the hardware one (a few
+  // ulp from the exactly rounded expression of Eq. (6)-(7))
+  const float cv = a.wv / ((mad_v + a.eps) * a.tau_v);
+  const float ct = a.wt / ((mad_t + a.eps) * a.tau_t);
   float sc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int i = e * kSelThreads + tid;
     const bool ok = i < N;
     const float sv = ok ? sv_p[i] : 0.f, st = ok ? st_p[i] : 0.f;
-    const float av = a.wv * (fmaxf((sv - med_v) / den_v, 0.f) / a.tau_v);
-    const float bt = a.wt * (fmaxf((st - med_t) / den_t, 0.f) / a.tau_t);
-    sc[e] = fmaxf(av, bt) + a.lam * sqrtf(av * bt);
+    const float dv = fmaxf(sv - med_v, 0.f), dt = fmaxf(st - med_t, 0.f);
+    const float av = dv > 0.f ? dv * cv : 0.f;  // clamped tokens stay exactly 0
+    const float bt = dt > 0.f ? dt * ct : 0.f;
+    sc[e] = fmaxf(av, bt) + a.lam * __builtin_amdgcn_sqrtf(av * bt);
     if (a.score_out && ok) a.score_out[(size_t)b * N + i] = sc[e];
   }
   block_topk_write<E>(sc, N, a.K, a.kept_idx + (size_t)b * a.K, sh);
