@@ -331,11 +331,28 @@ static_assert(kStreamR128 >= 2 && kStreamR128 <= 4 && kStreamR64 >= 2 && kStream
 // Physical 16-byte chunk of logical chunk c in row r of a 128-byte slab row.
 __device__ __forceinline__ int slab_swizzle(int r, int c) { return c ^ ((r >> 1) & 7); }
 
+#ifndef TREVS_STREAM_TG128
+#define TREVS_STREAM_TG128 2
+#endif
+// Text groups of the stream kernel's waves: with TG groups, wave w multiplies
+// the 32*TG tokens of group w % (8/TG) against the MT/TG text rows of group
+// w / (8/TG).  Larger per-wave tiles read fewer fragment bytes from LDS per
+// multiply (TG = 2 at 128 text rows: 16 KB per wave and stage, not 20 KB).
+template <int MT>
+struct StreamTiling {
+  static constexpr int TG = MT == 128 ? TREVS_STREAM_TG128 : 1;
+  static constexpr int ZB = TG;             // 32-token blocks per wave
+  static constexpr int MBW = MT / 32 / TG;  // 32-row text blocks per wave
+};
+
 template <class In, int MT, int R>
 __global__ __launch_bounds__(64 * kStreamWaves) void relevance_stream_kernel(RelArgs a) {
   constexpr int NT = 64 * kStreamWaves;
   constexpr int VT = kStreamTokens;
-  constexpr int MB = MT / 32;
+  constexpr int TG = StreamTiling<MT>::TG;
+  constexpr int ZB = StreamTiling<MT>::ZB;
+  constexpr int MBW = StreamTiling<MT>::MBW;
+  constexpr int NTG = kStreamWaves / TG;       // token groups
   constexpr int ZBYTES = VT * 128;
   constexpr int STAGE = ZBYTES + MT * 128;
   constexpr int ZPT = ZBYTES / 16 / NT;        // Z chunks per thread per stage
@@ -344,6 +361,7 @@ __global__ __launch_bounds__(64 * kStreamWaves) void relevance_stream_kernel(Rel
   static_assert(ZPT * NT * 16 == ZBYTES && TPT * NT * 16 == MT * 128, "stage split");
   __shared__ __attribute__((aligned(1024))) uint8_t l0[STAGE], l1[STAGE];
   __shared__ float tn[MT];
+  __shared__ float rpart[TG][VT];  // per-text-group row sums of Eq. (5)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
@@ -371,10 +389,12 @@ __global__ __launch_bounds__(64 * kStreamWaves) void relevance_stream_kernel(Rel
   }
   const int sdst = cr * 128 + slab_swizzle(cr, cc) * 16;
   const uint8_t* tbase = reinterpret_cast<const uint8_t*>(a.T) + (size_t)b * a.M_max * rb;
-  const int tok = tok0 + wave * 32 + col;
-  const int zr = wave * 32 + col;  // this lane's Z row in the stage
+  const int tgi = wave % NTG, xg = wave / NTG;  // token group, text group
+  // this lane's Z rows in the stage (token block zb): tgi*32*ZB + zb*32 + col
 
-  float zsq = 0.f, rsum = 0.f;
+  float zsq[ZB], rsum[ZB];
+#pragma unroll
+  for (int zb = 0; zb < ZB; ++zb) zsq[zb] = rsum[zb] = 0.f;
   for (int j0 = 0; j0 < Mb; j0 += MT) {
     const bool first = j0 == 0;
     if (!first) {  // the previous chunk's epilogue has read its norms
@@ -404,28 +424,37 @@ __global__ __launch_bounds__(64 * kStreamWaves) void relevance_stream_kernel(Rel
       for (int k = 0; k < TPT; ++k)
         *reinterpret_cast<u32x4*>(st + ZBYTES + sdst + k * (NT / 8) * 128) = src[ZPT + k];
     };
-    f32x16 acc[MB];
+    f32x16 acc[ZB][MBW];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+    for (int zb = 0; zb < ZB; ++zb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mb][r] = 0.f;
+      for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[zb][mb][r] = 0.f;
     auto compute = [&](const uint8_t* st) {
-      u32x4 zf[4];
+      u32x4 zf[ZB][4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        zf[q] = *reinterpret_cast<const u32x4*>(st + zr * 128 + slab_swizzle(zr, 4 * half + q) * 16);
-      if (j0 == 0) {
+      for (int zb = 0; zb < ZB; ++zb) {
+        const int zr = (tgi * ZB + zb) * 32 + col;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) zsq += sumsq(zf[q], In{});
+        for (int q = 0; q < 4; ++q)
+          zf[zb][q] = *reinterpret_cast<const u32x4*>(st + zr * 128 + slab_swizzle(zr, 4 * half + q) * 16);
+      }
+      if (j0 == 0 && xg == 0) {  // ||z||^2 once per token
+#pragma unroll
+        for (int zb = 0; zb < ZB; ++zb)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) zsq[zb] += sumsq(zf[zb][q], In{});
       }
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const int row = mb * 32 + col;
+      for (int mb = 0; mb < MBW; ++mb) {
+        const int row = (xg * MBW + mb) * 32 + col;
         u32x4 af[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           af[q] = *reinterpret_cast<const u32x4*>(st + ZBYTES + row * 128 + slab_swizzle(row, 4 * half + q) * 16);
-        acc[mb] = mfma_frag(af, zf, acc[mb], In{});
+#pragma unroll
+        for (int zb = 0; zb < ZB; ++zb) acc[zb][mb] = mfma_frag(af, zf[zb], acc[zb][mb], In{});
       }
     };
 #pragma unroll
@@ -451,17 +480,34 @@ __global__ __launch_bounds__(64 * kStreamWaves) void relevance_stream_kernel(Rel
     // ---- epilogue of this text chunk: sum_j max(t_j.z_i / ||t_j||, 0)^2
     // (the staged norm is zero for rows past the text, which drops them)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+    for (int zb = 0; zb < ZB; ++zb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float c = fmaxf(acc[mb][r] * tn[mb * 32 + mfma_row(r, half)], 0.f);
-        rsum = fmaf(c, c, rsum);
-      }
+      for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float c = fmaxf(acc[zb][mb][r] * tn[(xg * MBW + mb) * 32 + mfma_row(r, half)], 0.f);
+          rsum[zb] = fmaf(c, c, rsum[zb]);
+        }
   }
-  const float zz = zsq + __shfl_xor(zsq, 32, 64);
-  const float rr = rsum + __shfl_xor(rsum, 32, 64);
-  const float iz = 1.f / fmaxf(sqrtf(zz), 1e-12f);
-  if (half == 0 && tok < N) a.rel[(size_t)b * N + tok] = sqrtf(rr * iz * iz / (float)Mb);
+  // row sums of the text groups meet in LDS (a fixed order of additions)
+#pragma unroll
+  for (int zb = 0; zb < ZB; ++zb) {
+    const float rr = rsum[zb] + __shfl_xor(rsum[zb], 32, 64);
+    if (half == 0) rpart[xg][(tgi * ZB + zb) * 32 + col] = rr;
+  }
+  __syncthreads();
+  if (xg == 0) {
+#pragma unroll
+    for (int zb = 0; zb < ZB; ++zb) {
+      const int t = (tgi * ZB + zb) * 32 + col;
+      float rr = rpart[0][t];
+#pragma unroll
+      for (int x = 1; x < TG; ++x) rr += rpart[x][t];
+      const float zz = zsq[zb] + __shfl_xor(zsq[zb], 32, 64);
+      const float iz = 1.f / fmaxf(sqrtf(zz), 1e-12f);
+      if (half == 0 && tok0 + t < N) a.rel[(size_t)b * N + tok0 + t] = sqrtf(rr * iz * iz / (float)Mb);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
