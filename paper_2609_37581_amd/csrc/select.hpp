@@ -334,12 +334,54 @@ __device__ void block_write_mask(uint32_t mask, int K, int32_t* out, SelectShare
 
 // Stable top-K: keep every element whose score is above the K-th largest and
 // the lowest-index elements equal to it, and write the kept indices in
-// ascending order to out[0..K).
+// ascending order to out[0..K).  After the threshold selection one scan does
+// the rest: element i goes to slot above(i) + min(ties(i), need), where
+// above(i) and ties(i) count the elements before i (in index order) above the
+// threshold and equal to it, and need is how many ties are kept.  The two
+// counts travel packed in one int (low and high 16 bits; N <= 32768).
 template <int E>
 __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* out,
                                  SelectShared& sh) {
-  const uint32_t mask = block_topk_mask<E>([&](int e) { return f2key(sc[e]); }, N, K, sh);
-  block_write_mask<E>(mask, K, out, sh);
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  auto valid = [&](int e) { return e * kSelThreads + tid < N; };
+  if (K <= 0) return;
+  if (K >= N) {
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (valid(e)) out[e * kSelThreads + tid] = e * kSelThreads + tid;
+    return;
+  }
+  auto keyf = [&](int e) { return f2key(sc[e]); };
+  uint32_t thr;
+  int less, eq;
+  block_select<E>(keyf, N, N - K, thr, less, eq, sh);
+  const int need = K - (N - less - eq);  // ties kept, lowest index first
+  auto lanes_below = [&](unsigned long long bal) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+  };
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const uint32_t k = keyf(e);
+    const unsigned long long ba = __ballot(valid(e) && k > thr);
+    const unsigned long long bt = __ballot(valid(e) && k == thr);
+    if (lane == 0) sh.wcnt[e * kSelWaves + wave] = __popcll(ba) | (__popcll(bt) << 16);
+  }
+  wcnt_scan(E * kSelWaves, sh);
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const uint32_t k = keyf(e);
+    const bool above = valid(e) && k > thr, tie = valid(e) && k == thr;
+    const unsigned long long ba = __ballot(above);
+    const unsigned long long bt = __ballot(tie);
+    const int base = sh.wcnt[e * kSelWaves + wave];
+    const int na = (base & 0xffff) + lanes_below(ba);  // above the threshold, before this element
+    const int nt = (base >> 16) + lanes_below(bt);     // ties before this element
+    if (above || (tie && nt < need)) {
+      const int pos = na + min(nt, need);
+      if (pos < K) out[pos] = e * kSelThreads + tid;  // exactly K kept; the bound guards memory
+    }
+  }
 }
 
 }  // namespace trevs
