@@ -89,6 +89,21 @@ def test_stage1_keep_extremes(k):
         assert (g["kept_idx"] == np.arange(w.N)).all()
 
 
+@pytest.mark.parametrize("k", [1, 12345, 32768])
+def test_stage1_max_tokens(k):
+    """The largest N one selection supports (32,768 tokens, 32 per selection
+    thread), keeping one token, a ragged count, or every token; text of
+    60-100 rows (the 128-row relevance tile with a ragged tail)."""
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=2, N=32768, K1=k, d=256, M_max=100,
+                                            text_len=("uniform", 60, 100), n_sal=40, n_qm=40)
+    print(f"[stage1] max tokens, K1={k}", flush=True)
+    inp = stage1_inputs(w)
+    g = run_gpu(inp, w)
+    check(inp, w, g, run_oracle(inp, w))
+    if k == w.N:
+        assert (g["kept_idx"] == np.arange(w.N)).all()
+
+
 def test_stage1_single_token_and_constant_inputs():
     w = WORKLOADS["llava15-b1-f32"].with_(B=1, N=1, K1=1, d=64, M_max=3, n_sal=0, n_qm=0)
     inp = stage1_inputs(w)
