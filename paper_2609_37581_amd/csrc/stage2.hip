@@ -275,7 +275,8 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
 // sample's queries and keys stay in that L2).  It first ranks the heads of
 // its sample by (u desc, h asc) and keeps the first n_keep: the
 // high-variance set H*, ascending (the sample's first tile also stores it).
-// Wave w owns the 32 text rows of block pass*QW + w and all V keys.  For each
+// Wave w owns the 32 text rows of block pass*QW + (w % QW) and the keys of
+// 32-token block w / QW (or all V keys with one wave per text block).  For each
 // selected head the pass's Q rows (QW*32 of them) and their row log-sum-exps
 // are staged in LDS with coalesced 16-byte loads (a 32-row MFMA operand read
 // straight from memory would touch 32 rows per instruction), one head ahead.
@@ -288,20 +289,28 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
 // ---------------------------------------------------------------------------
 constexpr int kMaxHeads = 256;
 
+// Waves per 32-row text block: with 64-token tiles two waves split the keys
+// (32 each) and share the staged Q rows, two waves per SIMD (23 us against
+// 26 us with one wave per text block at the 16,384-token workload).
+#ifndef TREVS_SCORE_WPB
+#define TREVS_SCORE_WPB 2
+#endif
 template <int ROWB>
 struct ScoreTile {
   static constexpr int VB = ROWB <= 256 ? 2 : 1;  // 32-token blocks per workgroup
   static constexpr int V = 32 * VB;
+  static constexpr int WPB = VB == 2 ? TREVS_SCORE_WPB : 1;  // waves per 32-row text block
 };
 
 template <class In, int DH, int QW>
-__global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(64 * QW * ScoreTile<DH * In::kBytes>::WPB) void t2v_score_kernel(ScoreArgs a) {
   constexpr int ROWB = DH * In::kBytes;
   constexpr int HALFB = ROWB / 2;
   constexpr int NF = HALFB / 64;
-  constexpr int VB = ScoreTile<ROWB>::VB;
+  constexpr int WPB = ScoreTile<ROWB>::WPB;
+  constexpr int VB = ScoreTile<ROWB>::VB / WPB;  // 32-token blocks per wave
   constexpr int V = ScoreTile<ROWB>::V;
-  constexpr int NT = 64 * QW;
+  constexpr int NT = 64 * QW * WPB;
   constexpr int LROW = ROWB + 16;
   constexpr int CPR = ROWB / 16;
   constexpr int QR = 32 * QW;                  // text rows of a pass
@@ -315,7 +324,8 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
   __shared__ float u_lds[kMaxHeads];
   __shared__ int sel_lds[kMaxHeads];
   __shared__ int heads[kMaxHeads];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int wave = wv % QW, vw = wv / QW;  // text block of the pass, key blocks vw*VB..
   const int half = lane >> 5, col = lane & 31;
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int b = lin / a.n_vtiles, i0 = (lin - b * a.n_vtiles) * V;
@@ -329,7 +339,7 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
     heads[h] = 0;
   }
   __syncthreads();
-  for (int h = wave; h < Hq; h += QW) {
+  for (int h = wv; h < Hq; h += QW * WPB) {
     const float u = u_lds[h];
     int rank = 0;
     for (int c0 = 0; c0 < Hq; c0 += 64) {
@@ -340,7 +350,7 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
     if (lane == 0) sel_lds[h] = rank < nk;
   }
   __syncthreads();
-  if (wave == 0) {
+  if (wv == 0) {
     int base = 0;
     for (int c0 = 0; c0 < Hq; c0 += 64) {
       const int h = c0 + lane;
@@ -434,7 +444,7 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
       for (int j = 0; j < 4; ++j) lse[j] = *reinterpret_cast<const float4*>(&llds[qbuf][wave * 32 + 8 * j + 4 * half]);
 #pragma unroll
       for (int vb = 0; vb < VB; ++vb) {
-        const uint8_t* p = &klds[kbuf][(vb * 32 + col) * LROW + half * HALFB];
+        const uint8_t* p = &klds[kbuf][((vw * VB + vb) * 32 + col) * LROW + half * HALFB];
         f32x16 acc;
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) acc[rr] = 0.f;
@@ -493,11 +503,12 @@ __global__ __launch_bounds__(64 * QW) void t2v_score_kernel(ScoreArgs a) {
         if (r0 + wave * 32 + mfma_row(rr, half) < Tb) pm[vb] = fmaxf(pm[vb], accs[vb][rr]);
     __syncthreads();  // the next pass restages every buffer
   }
-  // operand A = text rows: a lane holds text rows of visual column (vb*32 + col)
+  // operand A = text rows: a lane holds text rows of visual column
+  // ((vw * VB + vb) * 32 + col)
 #pragma unroll
   for (int vb = 0; vb < VB; ++vb) {
     const float v = fmaxf(pm[vb], __shfl_xor(pm[vb], 32, 64));
-    if (half == 0) pmax[wave][vb * 32 + col] = v;
+    if (half == 0) pmax[wave][(vw * VB + vb) * 32 + col] = v;
   }
   __syncthreads();
   for (int t = tid; t < V; t += NT) {
@@ -578,17 +589,17 @@ static void launch_score_t(const ScoreArgs& a, hipStream_t s) {
   const int qw = score_qblocks(a.T_max, ROWB);
   if constexpr (ROWB <= 256) {
     if (qw == 4) {
-      hipLaunchKernelGGL((t2v_score_kernel<In, DH, 4>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((t2v_score_kernel<In, DH, 4>), grid, dim3(256 * ScoreTile<ROWB>::WPB), 0, s, a);
       return;
     }
   }
   if constexpr (ROWB <= 512) {
     if (qw == 2) {
-      hipLaunchKernelGGL((t2v_score_kernel<In, DH, 2>), grid, dim3(128), 0, s, a);
+      hipLaunchKernelGGL((t2v_score_kernel<In, DH, 2>), grid, dim3(128 * ScoreTile<ROWB>::WPB), 0, s, a);
       return;
     }
   }
-  hipLaunchKernelGGL((t2v_score_kernel<In, DH, 1>), grid, dim3(64), 0, s, a);
+  hipLaunchKernelGGL((t2v_score_kernel<In, DH, 1>), grid, dim3(64 * ScoreTile<ROWB>::WPB), 0, s, a);
 }
 
 template <class In>
