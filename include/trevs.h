@@ -25,7 +25,9 @@
  *   - Arguments are validated on the host before anything is launched;
  *     invalid arguments return an error and launch nothing.  Values that live
  *     in device memory (text lengths) cannot be checked without a device
- *     synchronisation: out-of-range values there are undefined behaviour.
+ *     synchronisation: the kernels clamp a text length into 1..M_max (or
+ *     1..T_max), so an out-of-range length computes with the nearest valid
+ *     one and never reads or writes outside the buffers.
  *   - Inputs must be finite.  Output buffers must not overlap the inputs or
  *     each other.  Outputs are undefined when an error is returned.
  *   - Index lists are int32, ascending and unique.  Top-K order is score

@@ -79,7 +79,7 @@ __global__ __launch_bounds__(64 * QW) void t2v_profile_kernel(ProfileArgs a) {
     }
   };
 
-  const int Tb = a.text_len ? a.text_len[b] : a.T_max;
+  const int Tb = text_rows(a.text_len, b, a.T_max);
   const int n_qblk = (Tb + 31) / 32;
   const int n_pass = (n_qblk + QW - 1) / QW;  // uniform over the workgroup (barriers below)
   const int n_iter = (n_tiles + RING - 1) / RING;

@@ -95,6 +95,13 @@ __device__ __forceinline__ void stg16_stream(void* p, u32x4 v) {
 
 __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 
+// Valid text rows of sample b: len[b] clamped into 1..rows (rows when len is
+// null).  The lengths live in device memory and cannot be validated on the
+// host; clamping keeps every access of a bad length inside the buffers.
+__device__ __forceinline__ int text_rows(const int32_t* len, int b, int rows) {
+  return len ? min(max(len[b], 1), rows) : rows;
+}
+
 // Word 3 of a raw (unstructured, stride 0) buffer resource on gfx9-family
 // GPUs: 32-bit data format, bounds checked against num_records.
 constexpr int kBufferRsrcWord3 = 0x00020000;

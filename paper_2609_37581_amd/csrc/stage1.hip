@@ -99,7 +99,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
   const int r = ((int)blockIdx.x - a.n_cls_blocks) * NWV + wave;  // = b*M_max + j
   if (r >= a.B * a.M_max) return;
   const int b = r / a.M_max, j = r - b * a.M_max;
-  const int Mb = a.text_len ? a.text_len[b] : a.M_max;
+  const int Mb = text_rows(a.text_len, b, a.M_max);
   float inv = 0.f;
   if (j < Mb) {
     const uint8_t* row = reinterpret_cast<const uint8_t*>(a.text) + (size_t)r * a.row_bytes;
@@ -190,7 +190,7 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
   const int b = tile / a.tiles_per_sample;
   const int tok0 = (tile - b * a.tiles_per_sample) * VT;
   const int N = a.N, rb = a.row_bytes;
-  const int Mb = a.text_len ? a.text_len[b] : a.M_max;
+  const int Mb = text_rows(a.text_len, b, a.M_max);
   const int n_slabs = (rb + SB - 1) / SB;
   const int n_pairs = (n_slabs + 1) / 2;
 
@@ -379,7 +379,7 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
   const int b = tile / a.tiles_per_sample;
   const int tok0 = (tile - b * a.tiles_per_sample) * VT;
   const int N = a.N, rb = a.row_bytes;
-  const int Mb = a.text_len ? a.text_len[b] : a.M_max;
+  const int Mb = text_rows(a.text_len, b, a.M_max);
   const int n_slabs = rb >> 7;
   const int n_iter = (n_slabs + U - 1) / U;  // stages padded to the unroll
 

@@ -216,7 +216,7 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
   __shared__ float red[kHeadThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = blockIdx.x, b = blockIdx.y;
-  const int Tb = a.text_len ? a.text_len[b] : a.T_max;
+  const int Tb = text_rows(a.text_len, b, a.T_max);
   const float invK = 1.f / (float)a.K_in;
   float vs = 0.f;
   for (int q = tid; q < a.T_max; q += kHeadThreads) {
@@ -368,7 +368,7 @@ __global__ __launch_bounds__(64 * QW * ScoreTile<DH * In::kBytes>::WPB) void t2v
   __syncthreads();
   auto head_at = [&](int hi) { return min(max(heads[min(hi, nk - 1)], 0), Hq - 1); };
 
-  const int Tb = a.text_len ? a.text_len[b] : a.T_max;
+  const int Tb = text_rows(a.text_len, b, a.T_max);
   const size_t seq0 = (size_t)b * a.S;
   const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k) + (seq0 + a.P) * a.H_kv * ROWB;
   const size_t kstride = (size_t)a.H_kv * ROWB;

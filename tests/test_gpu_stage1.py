@@ -104,6 +104,19 @@ def test_stage1_max_tokens(k):
         assert (g["kept_idx"] == np.arange(w.N)).all()
 
 
+def test_stage1_text_lengths_out_of_range_are_clamped():
+    """Text lengths live in device memory and are not validated on the host;
+    the kernels clamp them into 1..M_max, so 0 and M_max + 5 behave as 1 and
+    M_max (bit for bit)."""
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=2)
+    inp = stage1_inputs(w)
+    bad = dict(inp, text_len=np.array([0, w.M_max + 5], dtype=np.int32))
+    good = dict(inp, text_len=np.array([1, w.M_max], dtype=np.int32))
+    a, b = run_gpu(bad, w), run_gpu(good, w)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+
+
 def test_stage1_single_token_and_constant_inputs():
     w = WORKLOADS["llava15-b1-f32"].with_(B=1, N=1, K1=1, d=64, M_max=3, n_sal=0, n_qm=0)
     inp = stage1_inputs(w)

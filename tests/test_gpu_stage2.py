@@ -159,6 +159,17 @@ def test_stage2_max_visual_rows(k_keep):
         assert np.array_equal(g["hidden_out"], inp["hidden"])
 
 
+def test_stage2_text_lengths_out_of_range_are_clamped():
+    """Device-resident text lengths are clamped into 1..T_max by the kernels:
+    0 and T_max + 7 behave as 1 and T_max (bit for bit)."""
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=2)
+    inp = stage2_inputs(w)
+    a = run_gpu(dict(inp, text_len=np.array([0, w.T_max + 7], dtype=np.int32)), w)
+    b = run_gpu(dict(inp, text_len=np.array([1, w.T_max], dtype=np.int32)), w)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+
+
 @pytest.fixture(scope="module")
 def qwen_full():
     w = WORKLOADS["qwen25vl-b4-bf16"]
