@@ -22,9 +22,16 @@ namespace trevs {
 // in LDS; after the tile's barrier the first 32 threads add the waves' sums
 // in a fixed order into the split's running column sums (deterministic).
 // ---------------------------------------------------------------------------
-// Key tiles in flight: about eight 16-byte vectors per thread in registers.
+// Key tiles in flight: about TREVS_PROFILE_RING_VECS 16-byte vectors per
+// thread in registers.  A shallow ring keeps the kernel at 111 VGPRs, four
+// waves per SIMD, which hides the loads better than a deep ring at two
+// waves per SIMD (30.6 us against 38.3 us at the 16,384-token workload).
+#ifndef TREVS_PROFILE_RING_VECS
+#define TREVS_PROFILE_RING_VECS 2
+#endif
 constexpr int profile_ring(int vectors_per_tile) {
-  return vectors_per_tile >= 8 ? 1 : (vectors_per_tile >= 4 ? 2 : 8 / vectors_per_tile);
+  return vectors_per_tile >= TREVS_PROFILE_RING_VECS ? 1
+                                                     : TREVS_PROFILE_RING_VECS / vectors_per_tile;
 }
 
 template <class In, int DH, int QW>
