@@ -474,6 +474,7 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
     ga.row_bytes = a->d * e;
     ga.n_tiles = (a->N + 127) / 128;
     ga.G = reinterpret_cast<float*>(w + L.gram);
+    ga.inv_norm = reinterpret_cast<float*>(w + L.inv_norm);
     FpsArgs fa;
     fa.G = ga.G;
     fa.pivots = pivots;

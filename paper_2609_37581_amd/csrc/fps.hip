@@ -14,14 +14,17 @@
 namespace trevs {
 
 // ---------------------------------------------------------------------------
-// Gram matrix.  A workgroup of 4 waves computes a 128x128 tile of G[b]
-// (rows j of the tile's first operand, columns i of the second), streaming
-// the feature dimension in 128-byte slabs: each thread loads its share of
-// both slabs with coalesced 16-byte loads (8 lanes per 128-byte row
-// segment) into a ring of two register buffers, writes them to one of two
-// LDS buffers (rows XOR-swizzled by 16-byte chunk), and the waves multiply
-// on the matrix cores, each a 64x64 block.  Bytes past a row's end (a
-// partial last slab) load as zero.
+// Gram matrix.  G is symmetric, so only the tiles (tj, ti) with tj <= ti are
+// computed: a workgroup of 4 waves computes the 128x128 tile of G[b] (rows j
+// of the tile's first operand, columns i of the second), streaming the
+// feature dimension in 128-byte slabs: each thread loads its share of both
+// slabs with coalesced 16-byte loads (8 lanes per 128-byte row segment) into
+// a ring of two register buffers, writes them to one of two LDS buffers
+// (rows XOR-swizzled by 16-byte chunk), and the waves multiply on the matrix
+// cores, each a 64x64 block.  Bytes past a row's end (a partial last slab)
+// load as zero.  The tile is written in place and, off the diagonal, also
+// transposed through LDS (rows padded to 129 floats) with coalesced stores.
+// Diagonal tiles also write 1/max(||z_i||, 1e-12) from G_ii.
 // ---------------------------------------------------------------------------
 constexpr int kGramTile = 128;
 constexpr int kGramThreads = 256;
@@ -33,13 +36,24 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   constexpr int T = kGramTile;
   constexpr int SLAB = T * 128;                  // bytes of one operand slab
   constexpr int VPT = SLAB / 16 / kGramThreads;  // vectors per thread per operand
-  __shared__ __attribute__((aligned(1024))) uint8_t l0[2 * SLAB], l1[2 * SLAB];
+  constexpr int TP = T + 1;                      // padded row of the staged tile (floats)
+  constexpr int LDS = 4 * SLAB > T * TP * 4 ? 4 * SLAB : T * TP * 4;
+  // two operand-slab buffers during the product, then the finished tile
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS];
+  uint8_t* l0 = lds;
+  uint8_t* l1 = lds + 2 * SLAB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int nT = a.n_tiles;
+  const int n_pairs = nT * (nT + 1) / 2;
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
-  const int b = lin / (nT * nT), t2 = lin - b * nT * nT;
-  const int tj = t2 / nT, ti = t2 - tj * nT;
+  const int b = lin / n_pairs;
+  int tj = 0, rem = lin - b * n_pairs;  // upper-triangle pair (tj <= ti), row-major
+  while (rem >= nT - tj) {
+    rem -= nT - tj;
+    ++tj;
+  }
+  const int ti = tj + rem;
   const int N = a.N, rb = a.row_bytes;
   const int n_slabs = (rb + 127) / 128;
   const uint8_t* zb = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
@@ -126,29 +140,75 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
         if (i < N && j < N) gb[(size_t)j * N + i] = acc[m][n][r];
       }
     }
+  if (tj == ti) {  // the diagonal tile holds ||z_i||^2
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int jl = wj * 64 + m * 32 + mfma_row(r, half), il = wi * 64 + n * 32 + col;
+          const int i = ti * T + il;
+          if (jl == il && i < N)
+            a.inv_norm[(size_t)b * N + i] = 1.f / fmaxf(sqrtf(fmaxf(acc[m][n][r], 0.f)), 1e-12f);
+        }
+    return;
+  }
+  // the mirrored tile G[i, j] through LDS: stage tile[jl][il], then write
+  // rows il with consecutive jl per lane
+  __syncthreads();  // every wave is done with the operand slabs
+  float* tile = reinterpret_cast<float*>(lds);
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        tile[(wj * 64 + m * 32 + mfma_row(r, half)) * TP + wi * 64 + n * 32 + col] = acc[m][n][r];
+  __syncthreads();
+  for (int e = tid; e < T * T; e += kGramThreads) {
+    const int il = e / T, jl = e - il * T;
+    const int i = ti * T + il, j = tj * T + jl;
+    if (i < N && j < N) gb[(size_t)i * N + j] = tile[jl * TP + il];
+  }
 }
 
 // ---------------------------------------------------------------------------
 // Initial distances: for every token i, 1 - max over the pivots j of
-// cos(z_i, z_j) = G_ij / (||z_i|| ||z_j||) (norms floored at 1e-12), and
-// 1/||z_i|| for the picks.
+// cos(z_i, z_j) = G_ij / (||z_i|| ||z_j||), with the inverse norms the Gram
+// pass wrote.  One thread per token; the pivot loop is unrolled so that
+// several row reads of G are in flight (a pivot's row is read at consecutive
+// columns by consecutive threads).
 // ---------------------------------------------------------------------------
 constexpr int kFpsInitThreads = 256;
 
 __global__ __launch_bounds__(kFpsInitThreads) void fps_init_kernel(FpsArgs a) {
-  const int b = blockIdx.y, i = blockIdx.x * kFpsInitThreads + threadIdx.x, N = a.N;
-  if (i >= N) return;
+  const int b = blockIdx.y, N = a.N;
+  const int i = min((int)(blockIdx.x * kFpsInitThreads + threadIdx.x), N - 1);
   const float* gb = a.G + (size_t)b * N * N;
-  const float iz = 1.f / fmaxf(sqrtf(fmaxf(gb[(size_t)i * N + i], 0.f)), 1e-12f);
+  const float* inb = a.inv_norm + (size_t)b * N;
   const int32_t* piv = a.pivots + (size_t)b * a.K_r;
+  constexpr int U = 8;
   float mx = -INFINITY;
-  for (int p = 0; p < a.K_r; ++p) {
-    const int j = piv[p];
-    const float izj = 1.f / fmaxf(sqrtf(fmaxf(gb[(size_t)j * N + j], 0.f)), 1e-12f);
-    mx = fmaxf(mx, gb[(size_t)j * N + i] * iz * izj);
+  int p = 0;
+  for (; p + U <= a.K_r; p += U) {
+    int j[U];
+    float g[U], izj[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) j[u] = piv[p + u];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      g[u] = gb[(size_t)j[u] * N + i];
+      izj[u] = inb[j[u]];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) mx = fmaxf(mx, g[u] * izj[u]);
   }
-  a.dist[(size_t)b * N + i] = 1.f - mx;
-  a.inv_norm[(size_t)b * N + i] = iz;
+  for (; p < a.K_r; ++p) {
+    const int j = piv[p];
+    mx = fmaxf(mx, gb[(size_t)j * N + i] * inb[j]);
+  }
+  if (blockIdx.x * kFpsInitThreads + threadIdx.x < N) a.dist[(size_t)b * N + i] = 1.f - mx * inb[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -228,7 +288,7 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hipStream_t s) {
-  const dim3 ggrid(B * g.n_tiles * g.n_tiles);
+  const dim3 ggrid(B * g.n_tiles * (g.n_tiles + 1) / 2);
   if (dtype == 1)
     hipLaunchKernelGGL(gram_kernel<BF16>, ggrid, dim3(kGramThreads), 0, s, g);
   else

@@ -95,13 +95,14 @@ struct GramArgs {
   const void* Z;             // [B,N,d]
   int N, row_bytes, n_tiles; // n_tiles = ceil(N / 128)
   float* G;                  // [B,N,N] fp32 dot products z_j . z_i
+  float* inv_norm;           // [B,N] 1 / max(||z_i||, 1e-12)
 };
 struct FpsArgs {
   const float* G;            // [B,N,N]
   const int32_t* pivots;     // [B,K_r] ascending
   int N, K_r, K_d;
   float* dist;               // [B,N] work: distance to the selected set
-  float* inv_norm;           // [B,N] work: 1 / ||z_i||
+  float* inv_norm;           // [B,N] work: 1 / max(||z_i||, 1e-12), from the Gram pass
   int32_t* kept_idx;         // [B,K_r+K_d] ascending
   int32_t* div_idx;          // [B,K_d] picks in pick order, or null
 };
