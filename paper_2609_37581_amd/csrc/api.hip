@@ -52,7 +52,8 @@ trevs_status record(void* const* events, int slot, hipStream_t s) {
 
 // ------------------------------------------------------------------ stage 1
 struct PrellmLayout {
-  size_t row_stats, inv_tnorm, sal, rel, stats, pivots, gram, dist, inv_norm, total;
+  size_t row_stats, inv_tnorm, sal, rel, stats, rel_part, pivots, gram, dist, inv_norm, total;
+  RelPlan rel_plan;
 };
 
 trevs_status validate_prellm(const trevs_prellm_args* a) {
@@ -120,6 +121,9 @@ PrellmLayout prellm_layout(const trevs_prellm_args* a) {
   off = align_up(off + (size_t)a->B * a->N * sizeof(float));
   L.stats = off;
   off = align_up(off + (size_t)a->B * 4 * sizeof(float));
+  L.rel_plan = relevance_plan(a->B, a->N, a->M_max, a->d * elem_bytes(a->dtype));
+  L.rel_part = off;  // partial products of a feature-dimension split
+  off = align_up(off + L.rel_plan.part_floats() * sizeof(float));
   L.pivots = L.gram = L.dist = L.inv_norm = off;
   if (a->k_div > 0) {  // farthest point sampling: pivot list, Gram matrices, distances
     L.pivots = off;
@@ -421,13 +425,16 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   ra.N = a->N;
   ra.M_max = a->M_max;
   ra.row_bytes = a->d * e;
-  const int MT = a->M_max <= 32 ? 32 : (a->M_max <= 64 ? 64 : 128);
-  const int tile_tokens = relevance_tile_tokens_for(a->d * e, MT);
-  ra.tiles_per_sample = (a->N + tile_tokens - 1) / tile_tokens;
+  const RelPlan& rp = L.rel_plan;
+  ra.tiles_per_sample = rp.tiles_per_sample;
   ra.sal = sal;
   ra.rel = rel;
+  ra.n_split = rp.n_split;
+  ra.split_slabs = rp.split_slabs;
+  ra.part = reinterpret_cast<float*>(w + L.rel_part);
+  ra.zpart = ra.part + (size_t)rp.n_split * a->B * a->M_max * a->N;
   TREVS_TRY(record(a->events, 2, s));
-  TREVS_HIP(launch_relevance(ra, a->dtype, MT, s));
+  TREVS_HIP(launch_relevance(ra, rp, a->dtype, s));
   TREVS_TRY(record(a->events, 3, s));
 
   const bool budget = a->ratio_mode == TREVS_RATIO_BUDGET;

@@ -30,6 +30,24 @@ struct RelArgs {
   int B, N, M_max, row_bytes, tiles_per_sample;
   float* sal;                // [B,N]
   float* rel;                // [B,N]
+  // feature-dimension split (n_split > 1): workgroup (tile, split) covers
+  // the 128-byte slabs [split*split_slabs, ...) and writes its partial dot
+  // products t_j.z_i to part [B,n_split,M_max,N] and its partial ||z_i||^2
+  // to zpart [B,n_split,N]; a merge pass finishes Eq. (4)-(5)
+  int n_split, split_slabs;
+  float* part;
+  float* zpart;
+};
+
+// Launch shape of the relevance pass for one problem size.
+struct RelPlan {
+  bool stream;           // streaming kernel (rows of whole 128-byte slabs)
+  int MT;                // text rows per tile (32, 64 or 128)
+  int tile_tokens;       // visual tokens per workgroup
+  int tiles_per_sample;
+  int n_split, split_slabs;
+  size_t part_floats() const;  // floats of part + zpart (0 without a split)
+  int B, N, M_max;
 };
 
 struct NormArgs {
@@ -172,10 +190,8 @@ inline int select_e(int N) {
 }
 
 hipError_t launch_prep(const PrepArgs& a, int dtype, hipStream_t s);
-hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s);
-int relevance_tile_tokens();
-// Tokens per workgroup of the relevance launch for this row size / text tile.
-int relevance_tile_tokens_for(int row_bytes, int MT);
+RelPlan relevance_plan(int B, int N, int M_max, int row_bytes);
+hipError_t launch_relevance(const RelArgs& a, const RelPlan& p, int dtype, hipStream_t s);
 hipError_t launch_norm_stats(const NormArgs& a, int B, hipStream_t s);
 hipError_t launch_prellm_select(const SelArgs& a, int B, hipStream_t s);
 // Budget-split selection: the K_t highest s^t, then the K - K_t highest s^v

@@ -1,5 +1,7 @@
 // Stage 1 (pre-LLM) kernels: [CLS] saliency, textual relevance, robust
 // normalisation, fusion and pivot top-K (Sec. 4.1, Eq. (2)-(7)).
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "select.hpp"
@@ -301,9 +303,9 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Relevance, streaming variant for rows made of whole 128-byte slabs and a
-// text tile of 64 or 128 rows.  Same arithmetic as relevance_kernel; a
-// workgroup of 8 waves owns 256 tokens.  Stage s is the 128-byte slab s of
+// Relevance, streaming variant for rows made of whole 128-byte slabs (text
+// tiles of 32, 64 or 128 rows).  Same arithmetic as relevance_kernel; a
+// workgroup of 4, 8 or 16 waves owns 256 tokens.  Stage s is the 128-byte slab s of
 // the 256 Z rows and of the MT text rows.  Every thread loads its share of a
 // stage with coalesced 16-byte loads (8 lanes cover one 128-byte row
 // segment) into a ring of R register buffers, so R stages are in flight; at
@@ -313,7 +315,8 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
 // direct-to-LDS copies).  Rows are XOR-swizzled in 16-byte chunks so that
 // both the stage writes and the MFMA fragment reads of 16 consecutive rows
 // hit distinct banks.  Saliency (Eq. (2)-(3)) is computed while the first
-// stages load.
+// stages load.  With SPLIT the workgroup covers one range of slabs and
+// writes raw partial products and ||z||^2 for relevance_merge_kernel.
 // ---------------------------------------------------------------------------
 constexpr int kStreamWaves = 8;
 constexpr int kStreamTokens = 32 * kStreamWaves;
@@ -355,8 +358,9 @@ struct StreamTiling {
   static_assert(ZB >= 1 && NTG * ZB == 8 && MBW * TG * 32 == MT, "stream tiling");
 };
 
-template <class In, int MT, int R, int NW>
-__global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
+// (two waves per SIMD at four waves a workgroup: two workgroups per CU)
+template <class In, int MT, int R, int NW, bool SPLIT>
+__global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void relevance_stream_kernel(RelArgs a) {
   constexpr int NT = 64 * NW;
   constexpr int VT = kStreamTokens;
   constexpr int TG = StreamTiling<MT, NW>::TG;
@@ -375,12 +379,17 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  // the splits of one token tile are consecutive workgroups (one XCD, so
+  // they share the text slabs in its L2)
+  const int wid = xcd_remap(blockIdx.x, gridDim.x);
+  const int tile = SPLIT ? wid / a.n_split : wid;
+  const int split = SPLIT ? wid - tile * a.n_split : 0;
   const int b = tile / a.tiles_per_sample;
   const int tok0 = (tile - b * a.tiles_per_sample) * VT;
   const int N = a.N, rb = a.row_bytes;
   const int Mb = text_rows(a.text_len, b, a.M_max);
-  const int n_slabs = rb >> 7;
+  const int s_begin = split * a.split_slabs;  // first slab of this split
+  const int n_slabs = SPLIT ? min(rb >> 7, s_begin + a.split_slabs) - s_begin : rb >> 7;
   const int n_iter = (n_slabs + U - 1) / U;  // stages padded to the unroll
 
   const float* itn = a.inv_tnorm + (size_t)b * a.M_max;
@@ -395,7 +404,8 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
 #pragma unroll
   for (int k = 0; k < ZPT; ++k) {
     const int r = cr + (NT / 8) * k;
-    zsrc[k] = reinterpret_cast<const uint8_t*>(a.Z) + ((size_t)b * N + min(tok0 + r, N - 1)) * rb + cc * 16;
+    zsrc[k] = reinterpret_cast<const uint8_t*>(a.Z) + ((size_t)b * N + min(tok0 + r, N - 1)) * rb +
+              s_begin * 128 + cc * 16;
   }
   const int sdst = cr * 128 + slab_swizzle(cr, cc) * 16;
   const uint8_t* tbase = reinterpret_cast<const uint8_t*>(a.T) + (size_t)b * a.M_max * rb;
@@ -407,7 +417,7 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
   for (int zb = 0; zb < ZB; ++zb) zsq[zb] = rsum[zb] = 0.f;
   for (int j0 = 0; j0 < Mb; j0 += MT) {
     const bool first = j0 == 0;
-    if (!first) {  // the previous chunk's epilogue has read its norms
+    if (!first && !SPLIT) {  // the previous chunk's epilogue has read its norms
       __syncthreads();
       stage_norms(j0);
     }
@@ -415,7 +425,7 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
       const int r = cr + (NT / 8) * k;
-      tsrc[k] = tbase + (size_t)min(j0 + r, a.M_max - 1) * rb + cc * 16;
+      tsrc[k] = tbase + (size_t)min(j0 + r, a.M_max - 1) * rb + s_begin * 128 + cc * 16;
     }
     // stage s into register buffer g; the padding stages past the last slab
     // re-read the last slab (still in L2) and are never multiplied
@@ -470,8 +480,8 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
 #pragma unroll
     for (int c = 0; c < R; ++c) load(c, g[c]);
     if (first) {
-      tile_saliency<In>(a, b, tok0, VT, NT, tid);
-      stage_norms(0);
+      if (split == 0) tile_saliency<In>(a, b, tok0, VT, NT, tid);
+      if (!SPLIT) stage_norms(0);
     }
     for (int it = 0; it < n_iter; ++it) {
 #pragma unroll
@@ -487,6 +497,21 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
       }
     }
     __syncthreads();  // the LDS buffers are refilled by the next text chunk
+    if constexpr (SPLIT) {  // partial products of the valid rows; 32 lanes write 128 bytes
+      float* pp = a.part + (size_t)(b * a.n_split + split) * a.M_max * N;
+#pragma unroll
+      for (int zb = 0; zb < ZB; ++zb) {
+        const int t = tok0 + (tgi * ZB + zb) * 32 + col;
+#pragma unroll
+        for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int j = j0 + (xg * MBW + mb) * 32 + mfma_row(r, half);
+            if (j < Mb && t < N) pp[(size_t)j * N + t] = acc[zb][mb][r];
+          }
+      }
+      continue;
+    }
     // ---- epilogue of this text chunk: sum_j max(t_j.z_i / ||t_j||, 0)^2
     // (the staged norm is zero for rows past the text, which drops them)
 #pragma unroll
@@ -498,6 +523,16 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
           const float c = fmaxf(acc[zb][mb][r] * tn[(xg * MBW + mb) * 32 + mfma_row(r, half)], 0.f);
           rsum[zb] = fmaf(c, c, rsum[zb]);
         }
+  }
+  if constexpr (SPLIT) {
+    if (xg == 0)
+#pragma unroll
+      for (int zb = 0; zb < ZB; ++zb) {
+        const int t = tok0 + (tgi * ZB + zb) * 32 + col;
+        const float zz = zsq[zb] + __shfl_xor(zsq[zb], 32, 64);
+        if (half == 0 && t < N) a.zpart[(size_t)(b * a.n_split + split) * N + t] = zz;
+      }
+    return;
   }
   // row sums of the text groups meet in LDS (a fixed order of additions)
 #pragma unroll
@@ -517,6 +552,60 @@ __global__ __launch_bounds__(64 * NW) void relevance_stream_kernel(RelArgs a) {
       const float iz = 1.f / fmaxf(sqrtf(zz), 1e-12f);
       if (half == 0 && tok0 + t < N) a.rel[(size_t)b * N + tok0 + t] = sqrtf(rr * iz * iz / (float)Mb);
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Relevance merge after a feature-dimension split: a workgroup owns 32
+// tokens of one sample, thread (g, t) the text rows g, g + 32, ... of token
+// t.  It adds the n_split partial products of each row in split order,
+// applies the inverse text norm, rectifies and squares (Eq. (4)); the row
+// sums meet in LDS and the first row group divides by ||z_i||^2 (summed over
+// the splits) and by the text length (Eq. (5)).
+// ---------------------------------------------------------------------------
+constexpr int kMergeTokens = 32, kMergeGroups = 32;
+
+// (64 registers: two workgroups per CU)
+__global__ __launch_bounds__(kMergeTokens * kMergeGroups, 8) void relevance_merge_kernel(RelArgs a) {
+  __shared__ float red[kMergeGroups][kMergeTokens + 1], zred[kMergeGroups][kMergeTokens + 1];
+  const int t = threadIdx.x % kMergeTokens, g = threadIdx.x / kMergeTokens;
+  const int b = blockIdx.y, N = a.N, S = a.n_split;
+  const int i = blockIdx.x * kMergeTokens + t, ic = min(i, N - 1);
+  const int Mb = text_rows(a.text_len, b, a.M_max);
+  // uniform split base plus a 32-bit lane offset: the loads take their
+  // address from scalar registers
+  const size_t sstride = (size_t)a.M_max * N;
+  const float* pb = a.part + (size_t)b * S * sstride;
+  const float* itn = a.inv_tnorm + (size_t)b * a.M_max;
+  float r = 0.f;
+  for (int j = g; j < Mb; j += kMergeGroups) {
+    const int off = j * N + ic;
+    float c = 0.f;
+    for (int s0 = 0; s0 < S; s0 += 16) {  // 16 loads in flight, added in split order
+      float v[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) v[k] = pb[min(s0 + k, S - 1) * sstride + off];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) c += s0 + k < S ? v[k] : 0.f;
+    }
+    c = fmaxf(c * itn[j], 0.f);
+    r = fmaf(c, c, r);
+  }
+  float z = 0.f;  // ||z_i||^2: split sp goes to row group sp % 32
+  const float* zb = a.zpart + (size_t)b * S * N;
+  for (int sp = g; sp < S; sp += kMergeGroups) z += zb[(size_t)sp * N + ic];
+  red[g][t] = r;
+  zred[g][t] = z;
+  __syncthreads();
+  if (g == 0 && i < N) {
+    float rr = red[0][t], zz = zred[0][t];
+#pragma unroll 4
+    for (int x = 1; x < kMergeGroups; ++x) {
+      rr += red[x][t];
+      zz += zred[x][t];
+    }
+    const float iz = 1.f / fmaxf(sqrtf(zz), 1e-12f);
+    a.rel[(size_t)b * N + i] = sqrtf(rr * iz * iz / (float)Mb);
   }
 }
 
@@ -661,7 +750,54 @@ hipError_t launch_prep(const PrepArgs& a, int dtype, hipStream_t s) {
   return hipGetLastError();
 }
 
-int relevance_tile_tokens() { return 32 * kRelNW; }
+// Feature-dimension split.  The stream kernel keeps one workgroup per CU at
+// text tiles of 64 or 128 rows and two at 32 rows; a grid with fewer token
+// tiles than half of that resident capacity (256 CUs) leaves compute units
+// idle, so each tile is split along the feature dimension into as many
+// slab ranges as kSplitRounds resident rounds hold, keeping at least
+// kSplitMinSlabs 128-byte slabs per range.  The partial products cost 8
+// bytes per (text row, token, split) of extra traffic plus a merge pass, which
+// pays only while compute units would otherwise stand idle.
+#ifndef TREVS_REL_SPLIT_ROUNDS
+#define TREVS_REL_SPLIT_ROUNDS 1
+#endif
+#ifndef TREVS_REL_SPLIT_MIN_SLABS
+#define TREVS_REL_SPLIT_MIN_SLABS 4
+#endif
+#ifndef TREVS_STREAM_R32
+#define TREVS_STREAM_R32 2
+#endif
+constexpr int kNumCUs = 256;
+constexpr int kSplitRounds = TREVS_REL_SPLIT_ROUNDS, kSplitMinSlabs = TREVS_REL_SPLIT_MIN_SLABS;
+constexpr int kStreamR32 = TREVS_STREAM_R32;
+
+size_t RelPlan::part_floats() const {
+  return n_split > 1 ? (size_t)n_split * B * ((size_t)M_max + 1) * N : 0;
+}
+
+RelPlan relevance_plan(int B, int N, int M_max, int row_bytes) {
+  RelPlan p;
+  p.B = B;
+  p.N = N;
+  p.M_max = M_max;
+  p.MT = M_max <= 32 ? 32 : (M_max <= 64 ? 64 : 128);
+  p.stream = row_bytes % 128 == 0;
+  p.tile_tokens = p.stream ? kStreamTokens : 32 * kRelNW;
+  p.tiles_per_sample = (N + p.tile_tokens - 1) / p.tile_tokens;
+  p.n_split = 1;
+  p.split_slabs = row_bytes / 128;
+  const long tiles = (long)B * p.tiles_per_sample;
+  const long resident = (long)kNumCUs * (p.MT == 32 ? 2 : 1);
+  if (p.stream && 2 * tiles <= resident) {
+    const int slabs = row_bytes / 128;
+    const int want = (int)std::min<long>(kSplitRounds * resident / tiles, std::max(slabs / kSplitMinSlabs, 1));
+    if (want > 1) {
+      p.split_slabs = (slabs + want - 1) / want;
+      p.n_split = (slabs + p.split_slabs - 1) / p.split_slabs;
+    }
+  }
+  return p;
+}
 
 template <class In>
 static void launch_rel_t(const RelArgs& a, int MT, hipStream_t s) {
@@ -674,33 +810,41 @@ static void launch_rel_t(const RelArgs& a, int MT, hipStream_t s) {
     hipLaunchKernelGGL((relevance_kernel<In, 128, kRelNW, kRelSB>), grid, block, 0, s, a);
 }
 
-bool relevance_uses_stream(int row_bytes, int MT) { return row_bytes % 128 == 0 && MT >= 64; }
-int relevance_tile_tokens_for(int row_bytes, int MT) {
-  return relevance_uses_stream(row_bytes, MT) ? kStreamTokens : relevance_tile_tokens();
-}
-
-template <class In>
+template <class In, bool SPLIT>
 static void launch_rel_stream_t(const RelArgs& a, int MT, hipStream_t s) {
-  const dim3 grid(a.B * a.tiles_per_sample);
+  const dim3 grid(a.B * a.tiles_per_sample * a.n_split);
   constexpr int NW128 = TREVS_STREAM_NW128;
-  if (MT == 64)
-    hipLaunchKernelGGL((relevance_stream_kernel<In, 64, kStreamR64, kStreamWaves>), grid,
+  if (MT == 32)
+    hipLaunchKernelGGL((relevance_stream_kernel<In, 32, kStreamR32, 4, SPLIT>), grid, dim3(64 * 4), 0, s, a);
+  else if (MT == 64)
+    hipLaunchKernelGGL((relevance_stream_kernel<In, 64, kStreamR64, kStreamWaves, SPLIT>), grid,
                        dim3(64 * kStreamWaves), 0, s, a);
   else
-    hipLaunchKernelGGL((relevance_stream_kernel<In, 128, kStreamR128, NW128>), grid, dim3(64 * NW128),
-                       0, s, a);
+    hipLaunchKernelGGL((relevance_stream_kernel<In, 128, kStreamR128, NW128, SPLIT>), grid,
+                       dim3(64 * NW128), 0, s, a);
 }
 
-hipError_t launch_relevance(const RelArgs& a, int dtype, int MT, hipStream_t s) {
-  if (relevance_uses_stream(a.row_bytes, MT)) {
+hipError_t launch_relevance(const RelArgs& a, const RelPlan& p, int dtype, hipStream_t s) {
+  if (!p.stream) {
     if (dtype == 1)
-      launch_rel_stream_t<BF16>(a, MT, s);
+      launch_rel_t<BF16>(a, p.MT, s);
     else
-      launch_rel_stream_t<F32>(a, MT, s);
+      launch_rel_t<F32>(a, p.MT, s);
+    return hipGetLastError();
+  }
+  if (p.n_split > 1) {
+    if (dtype == 1)
+      launch_rel_stream_t<BF16, true>(a, p.MT, s);
+    else
+      launch_rel_stream_t<F32, true>(a, p.MT, s);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid((a.N + kMergeTokens - 1) / kMergeTokens, a.B);
+    hipLaunchKernelGGL(relevance_merge_kernel, grid, dim3(kMergeTokens * kMergeGroups), 0, s, a);
   } else if (dtype == 1) {
-    launch_rel_t<BF16>(a, MT, s);
+    launch_rel_stream_t<BF16, false>(a, p.MT, s);
   } else {
-    launch_rel_t<F32>(a, MT, s);
+    launch_rel_stream_t<F32, false>(a, p.MT, s);
   }
   return hipGetLastError();
 }

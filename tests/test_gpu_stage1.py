@@ -60,6 +60,12 @@ CASES = {
     # more text rows than one 128-row chunk
     "long-text-bf16": WORKLOADS["llava15-b64-bf16"].with_(
         B=2, N=300, d=512, M_max=150, K1=100, n_sal=4, n_qm=6, text_len=("uniform", 129, 150)),
+    # grids of at least one 256-token tile per compute unit run unsplit, at
+    # text tiles of 64 and 32 rows
+    "unsplit-64rows-bf16": WORKLOADS["llava15-b64-bf16"].with_(B=96, d=256),
+    "unsplit-32rows-f32": WORKLOADS["llava15-b1-f32"].with_(B=96, d=256),
+    # a feature-dimension split whose last range is shorter (33 slabs in 7)
+    "split-uneven-f32": WORKLOADS["llava15-b1-f32"].with_(d=1056),
     "tie-stress-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=4, tie_stress=True),
     "rho0-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, rho=0.0),
     "rho0.25-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, rho=0.25),
