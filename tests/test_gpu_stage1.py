@@ -66,6 +66,8 @@ CASES = {
     "unsplit-32rows-f32": WORKLOADS["llava15-b1-f32"].with_(B=96, d=256),
     # a feature-dimension split whose last range is shorter (33 slabs in 7)
     "split-uneven-f32": WORKLOADS["llava15-b1-f32"].with_(d=1056),
+    # the batch-32 sweep shape at full size: 96 tiles split 5 ways
+    "split-sweep-b32-bf16": WORKLOADS["sweep-llava15-b32-bf16"],
     "tie-stress-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=4, tie_stress=True),
     "rho0-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, rho=0.0),
     "rho0.25-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, rho=0.25),
