@@ -142,7 +142,8 @@ PrellmLayout prellm_layout(const trevs_prellm_args* a) {
 // ------------------------------------------------------------------ stage 2
 struct InllmPlan {
   int n_split, split_len, n_rgroups, rest_len;
-  size_t part, part_rest, lse2, head_var, head_sel, score, total;
+  int n_vtiles, n_hsplit, hps;  // token-score tiles per sample, head splits, heads per split
+  size_t part, part_rest, lse2, head_var, head_sel, score, hpart, total;
 };
 
 trevs_status validate_inllm(const trevs_inllm_args* a) {
@@ -241,6 +242,13 @@ InllmPlan inllm_plan(const trevs_inllm_args* a) {
   off = align_up(off + (size_t)a->B * a->n_keep_heads * sizeof(int32_t));
   p.score = off;
   off = align_up(off + (size_t)a->B * a->K_in * sizeof(float));
+  const int vt = score_tile_tokens(a->dtype, a->d_head);
+  p.n_vtiles = (a->K_in + vt - 1) / vt;
+  const int hs = score_head_splits(a->B, p.n_vtiles, a->n_keep_heads);
+  p.hps = (a->n_keep_heads + hs - 1) / hs;
+  p.n_hsplit = (a->n_keep_heads + p.hps - 1) / p.hps;  // no split is empty
+  p.hpart = off;  // per-split head sums of the token-score pass
+  off = align_up(off + (p.n_hsplit > 1 ? (size_t)a->B * p.n_hsplit * a->T_max * a->K_in * sizeof(float) : 0));
   p.total = off;
   return p;
 }
@@ -583,7 +591,10 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   sa.H_kv = a->H_kv;
   sa.G = G;
   sa.n_keep = a->n_keep_heads;
-  sa.n_vtiles = (a->K_in + score_tile_tokens(a->dtype, a->d_head) - 1) / score_tile_tokens(a->dtype, a->d_head);
+  sa.n_vtiles = p.n_vtiles;
+  sa.n_hsplit = p.n_hsplit;
+  sa.hps = p.hps;
+  sa.hpart = reinterpret_cast<float*>(w + p.hpart);
   sa.scale_log2e = scale_log2e;
   sa.lse2 = lse2;
   sa.head_var = head_var;

@@ -106,6 +106,12 @@ struct ScoreArgs {
   int32_t* head_sel;         // [B,n_keep] H* ascending, or null
   const int32_t* text_len;
   float* p;                  // [B,K_in]
+  // head split (n_hsplit > 1): workgroup (tile, split) sums the attention of
+  // the selected heads [split*hps, (split+1)*hps) and writes it per (text
+  // row, token) to hpart [B,n_hsplit,T_max,K_in]; a merge pass adds the
+  // splits and takes the max over text rows
+  int n_hsplit, hps;
+  float* hpart;
 };
 
 // ---------------------------------------------------------------- diversity set
@@ -207,5 +213,7 @@ hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 int stats_waves(int G, int T_max);
 // Visual tokens per workgroup of the token-score pass.
 int score_tile_tokens(int dtype, int dh);
+// Head splits of the token-score pass (1: none).
+int score_head_splits(int B, int n_vtiles, int n_keep);
 
 }  // namespace trevs

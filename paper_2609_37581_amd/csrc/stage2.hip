@@ -327,9 +327,12 @@ __global__ __launch_bounds__(64 * QW * ScoreTile<DH * In::kBytes>::WPB) void t2v
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int wave = wv % QW, vw = wv / QW;  // text block of the pass, key blocks vw*VB..
   const int half = lane >> 5, col = lane & 31;
-  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  // the head splits of one tile are consecutive workgroups (one XCD)
+  const int lin0 = xcd_remap(blockIdx.x, gridDim.x);
+  const int lin = lin0 / a.n_hsplit, hs = lin0 - lin * a.n_hsplit;
   const int b = lin / a.n_vtiles, i0 = (lin - b * a.n_vtiles) * V;
   const int Hq = a.H_q, nk = a.n_keep;
+  const int h_lo = hs * a.hps, h_hi = min(nk, h_lo + a.hps);  // selected-head indices of this split
 
   // ---- high-variance head set H*: the rank of head h under (u desc, h asc)
   // counts the heads before it, 64 comparisons per ballot (wave w ranks heads
@@ -360,7 +363,7 @@ __global__ __launch_bounds__(64 * QW * ScoreTile<DH * In::kBytes>::WPB) void t2v
                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
       if (sel && pos < nk) {  // ranks are distinct for finite u
         heads[pos] = h;
-        if (i0 == 0 && a.head_sel) a.head_sel[(size_t)b * nk + pos] = h;
+        if (i0 == 0 && hs == 0 && a.head_sel) a.head_sel[(size_t)b * nk + pos] = h;
       }
       base += (int)__popcll(bal);
     }
@@ -467,27 +470,27 @@ __global__ __launch_bounds__(64 * QW * ScoreTile<DH * In::kBytes>::WPB) void t2v
     // group runs of H*: the first run's key tile goes to buffer 0, the next
     // run's tile waits in registers until its run starts
     u32x4 kst[KVT];
-    load_tile(head_at(0) / a.G, kst);
+    load_tile(head_at(h_lo) / a.G, kst);
     store_tile(0, kst);
-    int he = next_group(0);
-    if (he < nk) load_tile(head_at(he) / a.G, kst);
+    int he = next_group(h_lo);
+    if (he < h_hi) load_tile(head_at(he) / a.G, kst);
     int kbuf = 0;
     u32x4 qr[QVT];
     float4 lr;
-    load_q(0, qr, lr);
-    for (int hi = 0; hi < nk; hi += 2) {
+    load_q(h_lo, qr, lr);
+    for (int hi = h_lo; hi < h_hi; hi += 2) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const int h = hi + c;
-        if (h < nk) {  // uniform over the workgroup
+        if (h < h_hi) {  // uniform over the workgroup
           // Q buffer c was last read at head h - 2, before every wave passed
           // the barrier of head h - 1; a new group's key buffer was last
           // read two groups back, before the barrier of this group's start
-          if (h > 0 && h == he) {
+          if (h > h_lo && h == he) {
             kbuf ^= 1;
             store_tile(kbuf, kst);
             he = next_group(h);
-            if (he < nk) load_tile(head_at(he) / a.G, kst);
+            if (he < h_hi) load_tile(head_at(he) / a.G, kst);
           }
           store_q(c, qr, lr);
           __syncthreads();
@@ -496,13 +499,27 @@ __global__ __launch_bounds__(64 * QW * ScoreTile<DH * In::kBytes>::WPB) void t2v
         }
       }
     }
+    if (a.n_hsplit > 1) {  // this split's head sums of the valid rows; 32 lanes write 128 bytes
+      float* hp = a.hpart + ((size_t)b * a.n_hsplit + hs) * a.T_max * a.K_in;
 #pragma unroll
-    for (int vb = 0; vb < VB; ++vb)
+      for (int vb = 0; vb < VB; ++vb) {
+        const int i = i0 + (vw * VB + vb) * 32 + col;
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr)
-        if (r0 + wave * 32 + mfma_row(rr, half) < Tb) pm[vb] = fmaxf(pm[vb], accs[vb][rr]);
+        for (int rr = 0; rr < 16; ++rr) {
+          const int q = r0 + wave * 32 + mfma_row(rr, half);
+          if (q < Tb && i < a.K_in) hp[(size_t)q * a.K_in + i] = accs[vb][rr];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr)
+          if (r0 + wave * 32 + mfma_row(rr, half) < Tb) pm[vb] = fmaxf(pm[vb], accs[vb][rr]);
+    }
     __syncthreads();  // the next pass restages every buffer
   }
+  if (a.n_hsplit > 1) return;
   // operand A = text rows: a lane holds text rows of visual column
   // ((vw * VB + vb) * 32 + col)
 #pragma unroll
@@ -521,7 +538,54 @@ __global__ __launch_bounds__(64 * QW * ScoreTile<DH * In::kBytes>::WPB) void t2v
   }
 }
 
+// ---------------------------------------------------------------------------
+// Token-score merge after a head split: a workgroup owns 32 visual tokens of
+// one sample, thread (g, t) the text rows g, g + 8, ... of token t.  It adds
+// the splits' head sums of each row in split order and keeps the maximum
+// over the valid text rows; the row groups meet in LDS and the result is
+// divided by |H*| (Eq. (9)).
+// ---------------------------------------------------------------------------
+constexpr int kScoreMergeTokens = 32, kScoreMergeGroups = 8;
+
+__global__ __launch_bounds__(kScoreMergeTokens * kScoreMergeGroups) void t2v_score_merge_kernel(ScoreArgs a) {
+  __shared__ float red[kScoreMergeGroups][kScoreMergeTokens + 1];
+  const int t = threadIdx.x % kScoreMergeTokens, g = threadIdx.x / kScoreMergeTokens;
+  const int b = blockIdx.y, i = blockIdx.x * kScoreMergeTokens + t, ic = min(i, a.K_in - 1);
+  const int S = a.n_hsplit, Tb = text_rows(a.text_len, b, a.T_max);
+  // uniform split base plus a 32-bit lane offset
+  const size_t sstride = (size_t)a.T_max * a.K_in;
+  const float* pb = a.hpart + (size_t)b * S * sstride;
+  float best = 0.f;  // attention sums are nonnegative
+  for (int q = g; q < Tb; q += kScoreMergeGroups) {
+    const int off = q * a.K_in + ic;
+    float c = 0.f;
+    for (int s0 = 0; s0 < S; s0 += 8) {  // 8 loads in flight, added in split order
+      float v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = pb[min(s0 + k, S - 1) * sstride + off];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) c += s0 + k < S ? v[k] : 0.f;
+    }
+    best = fmaxf(best, c);
+  }
+  red[g][t] = best;
+  __syncthreads();
+  if (g == 0 && i < a.K_in) {
+    float v = red[0][t];
+#pragma unroll
+    for (int x = 1; x < kScoreMergeGroups; ++x) v = fmaxf(v, red[x][t]);
+    a.p[(size_t)b * a.K_in + i] = v / (float)a.n_keep;
+  }
+}
+
 // ---------------------------------------------------------------- launchers
+// Selected heads are split over workgroups while the tiles leave compute
+// units idle: up to one split per selected head, about one workgroup per CU.
+int score_head_splits(int B, int n_vtiles, int n_keep) {
+  const long tiles = (long)B * n_vtiles;
+  return (int)std::max<long>(1, std::min<long>(n_keep, 256 / tiles));
+}
+
 int stats_waves(int G, int T_max) {
   const int nrb = (G * T_max + 31) / 32;
   return nrb >= 8 ? 8 : (nrb >= 4 ? 4 : (nrb >= 2 ? 2 : 1));
@@ -584,7 +648,7 @@ int score_tile_tokens(int dtype, int dh) {
 
 template <class In, int DH>
 static void launch_score_t(const ScoreArgs& a, hipStream_t s) {
-  const dim3 grid(a.B * a.n_vtiles);
+  const dim3 grid(a.B * a.n_vtiles * a.n_hsplit);
   constexpr int ROWB = DH * In::kBytes;
   const int qw = score_qblocks(a.T_max, ROWB);
   if constexpr (ROWB <= 256) {
@@ -617,6 +681,12 @@ hipError_t launch_score(const ScoreArgs& a, int dtype, int dh, hipStream_t s) {
     launch_score_d<BF16>(a, dh, s);
   else
     launch_score_d<F32>(a, dh, s);
+  if (a.n_hsplit > 1) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid((a.K_in + kScoreMergeTokens - 1) / kScoreMergeTokens, a.B);
+    hipLaunchKernelGGL(t2v_score_merge_kernel, grid, dim3(kScoreMergeTokens * kScoreMergeGroups), 0, s, a);
+  }
   return hipGetLastError();
 }
 

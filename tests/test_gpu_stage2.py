@@ -79,6 +79,10 @@ CASES = {
     "bf16-dh256-mqa": WORKLOADS["llava15-b64-bf16"].with_(
         B=2, K1=130, K2=30, M_max=33, text_len=("uniform", 20, 33), H_q=8, H_kv=1, d_h=256,
         D=64, n_keep=3),
+    # token score: 192 tiles run unsplit; 96 tiles split the 5 selected heads
+    # 3 + 2 over two workgroups per tile
+    "b64-unsplit-score-bf16": WORKLOADS["llava15-b64-bf16"].with_(H_q=8, H_kv=8, n_keep=4, D=64),
+    "b32-head-split-score-bf16": WORKLOADS["sweep-llava15-b32-bf16"].with_(H_q=8, H_kv=8, n_keep=5, D=64),
 }
 
 
