@@ -197,7 +197,7 @@ trevs_status validate_inllm(const trevs_inllm_args* a) {
 }
 
 // Split of the visual keys for the statistics pass: enough workgroups to fill
-// the GPU (>= 2 per CU), each split at least 256 keys, lengths multiples of 64
+// the GPU (>= 2 per CU), each split at least 64 keys, lengths multiples of 64
 // (the pass consumes key tiles in pairs of 32).
 struct StatsPlan {
   int n_split, split_len, n_rgroups;
@@ -210,7 +210,7 @@ StatsPlan stats_plan(int B, int K_in, int T_max, int H_q, int H_kv, int softmax,
   const int nw = stats_waves(G, T_max);
   p.n_rgroups = (nrb + nw - 1) / nw;
   const int64_t base_wgs = (int64_t)B * H_kv * p.n_rgroups;
-  int n_split = (int)std::min<int64_t>((512 + base_wgs - 1) / base_wgs, (K_in + 255) / 256);
+  int n_split = (int)std::min<int64_t>((512 + base_wgs - 1) / base_wgs, (K_in + 63) / 64);
   n_split = std::max(n_split, 1);
   p.split_len = ((K_in + n_split - 1) / n_split + 63) / 64 * 64;
   p.n_split = (K_in + p.split_len - 1) / p.split_len;
