@@ -61,9 +61,12 @@ CASES = {
     "long-text-bf16": WORKLOADS["llava15-b64-bf16"].with_(
         B=2, N=300, d=512, M_max=150, K1=100, n_sal=4, n_qm=6, text_len=("uniform", 129, 150)),
     # grids of at least one 256-token tile per compute unit run unsplit, at
-    # text tiles of 64 and 32 rows
+    # text tiles of 64 and 32 rows; at 64 rows a 192-token tile is taken when
+    # it streams fewer rows per CU (the first case and the ragged one)
     "unsplit-64rows-bf16": WORKLOADS["llava15-b64-bf16"].with_(B=96, d=256),
     "unsplit-32rows-f32": WORKLOADS["llava15-b1-f32"].with_(B=96, d=256),
+    "tile192-ragged-bf16": WORKLOADS["llava15-b64-bf16"].with_(B=70, N=500, d=256, K1=150),
+    "tile256-64rows-bf16": WORKLOADS["llava15-b64-bf16"].with_(B=100, N=512, d=256, K1=128),
     # a feature-dimension split whose last range is shorter (33 slabs in 7)
     "split-uneven-f32": WORKLOADS["llava15-b1-f32"].with_(d=1056),
     # the batch-32 sweep shape at full size: 96 tiles split 5 ways
