@@ -305,8 +305,9 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
 // ---------------------------------------------------------------------------
 // Relevance, streaming variant for rows made of whole 128-byte slabs (text
 // tiles of 32, 64 or 128 rows).  Same arithmetic as relevance_kernel; a
-// workgroup of 4, 8 or 16 waves owns 256 tokens.  Stage s is the 128-byte slab s of
-// the 256 Z rows and of the MT text rows.  Every thread loads its share of a
+// workgroup of 4, 8 or 16 waves owns 256 tokens (12 waves own 192 tokens
+// at 64 text rows).  Stage s is the 128-byte slab s of the tile's Z rows and
+// of the MT text rows.  Every thread loads its share of a
 // stage with coalesced 16-byte loads (8 lanes cover one 128-byte row
 // segment) into a ring of R register buffers, so R stages are in flight; at
 // each step the oldest buffer is written to one of two LDS buffers, the
