@@ -96,6 +96,22 @@ def test_workspace_size_is_positive_for_valid_args():
     assert L.trevs_inllm_workspace_size(ctypes.byref(_inllm(softmax=1))) >= vis + 2 * 32 * 32 * 16
 
 
+def test_small_grids_reserve_split_partials():
+    """A grid with fewer tiles than compute units splits the relevance pass
+    over the feature dimension and the token score over the selected heads;
+    the partial sums those splits write live in the workspace, so its size
+    must cover at least two splits' worth."""
+    L = trevs.lib()
+    # 2 samples x 3 token tiles: split; 200 samples: one tile per CU or more
+    small = L.trevs_prellm_workspace_size(ctypes.byref(_prellm()))
+    big = L.trevs_prellm_workspace_size(ctypes.byref(_prellm(B=200)))
+    assert small >= 2 * 2 * (32 + 1) * 576 * 4  # [B, splits >= 2, M_max + 1, N] floats
+    assert big < 200 * 576 * 64                  # no partials: about 40 bytes per token
+    # token score: 2 samples x 3 tiles of 64 keys split the 16 selected heads
+    small = L.trevs_inllm_workspace_size(ctypes.byref(_inllm()))
+    assert small >= 2 * 2 * 32 * 192 * 4        # [B, splits >= 2, T_max, K_in] floats
+
+
 @pytest.mark.parametrize("bad,code", [
     (dict(k_keep=0), 1), (dict(k_keep=577), 1), (dict(n_seg=5), 1), (dict(d=4095), 1),
     (dict(textual_ratio=-0.1), 1), (dict(textual_ratio=float("nan")), 1), (dict(tau_v=0.0), 1),
