@@ -29,6 +29,19 @@ namespace trevs {
 constexpr int kGramTile = 128;
 constexpr int kGramThreads = 256;
 
+// Workgroup order: the tile pairs are walked in super-blocks of gs x gs
+// tiles (gs = min(8, tiles per side)), so that the ~64 workgroups resident on
+// one XCD at a time share 2*gs row blocks of Z and each slab they stream is
+// reused from L2 by gs workgroups (in row-major tile order they shared one
+// row block and streamed 64 distinct ones).  Super-blocks on and above the
+// diagonal are numbered row-major; a slot below the diagonal (or past the
+// last tile) exits at once.
+__host__ __device__ constexpr int gram_super(int n_tiles) { return n_tiles < 8 ? n_tiles : 8; }
+__host__ __device__ constexpr int gram_super_pairs(int n_tiles) {
+  return ((n_tiles + gram_super(n_tiles) - 1) / gram_super(n_tiles)) *
+         ((n_tiles + gram_super(n_tiles) - 1) / gram_super(n_tiles) + 1) / 2;
+}
+
 __device__ __forceinline__ int gram_swizzle(int r, int c) { return c ^ ((r >> 1) & 7); }
 
 template <class In>
@@ -45,15 +58,18 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int nT = a.n_tiles;
-  const int n_pairs = nT * (nT + 1) / 2;
+  const int gs = gram_super(nT), nS = (nT + gs - 1) / gs;
+  const int per_b = gram_super_pairs(nT) * gs * gs;
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
-  const int b = lin / n_pairs;
-  int tj = 0, rem = lin - b * n_pairs;  // upper-triangle pair (tj <= ti), row-major
-  while (rem >= nT - tj) {
-    rem -= nT - tj;
-    ++tj;
+  const int b = lin / per_b;
+  const int rem = lin - b * per_b, sp = rem / (gs * gs), loc = rem - sp * gs * gs;
+  int sj = 0, rs = sp;  // super-block pair (sj <= si), row-major
+  while (rs >= nS - sj) {
+    rs -= nS - sj;
+    ++sj;
   }
-  const int ti = tj + rem;
+  const int tj = sj * gs + loc / gs, ti = (sj + rs) * gs + loc % gs;
+  if (tj > ti || ti >= nT) return;  // the whole workgroup: no barrier has run
   const int N = a.N, rb = a.row_bytes;
   const int n_slabs = (rb + 127) / 128;
   const uint8_t* zb = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
@@ -288,7 +304,7 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hipStream_t s) {
-  const dim3 ggrid(B * g.n_tiles * (g.n_tiles + 1) / 2);
+  const dim3 ggrid(B * gram_super_pairs(g.n_tiles) * gram_super(g.n_tiles) * gram_super(g.n_tiles));
   if (dtype == 1)
     hipLaunchKernelGGL(gram_kernel<BF16>, ggrid, dim3(kGramThreads), 0, s, g);
   else
