@@ -247,6 +247,10 @@ InllmPlan inllm_plan(const trevs_inllm_args* a) {
   const int hs = score_head_splits(a->B, p.n_vtiles, a->n_keep_heads);
   p.hps = (a->n_keep_heads + hs - 1) / hs;
   p.n_hsplit = (a->n_keep_heads + p.hps - 1) / p.hps;  // no split is empty
+  if ((size_t)a->B * p.n_hsplit * a->T_max * a->K_in * sizeof(float) > (size_t(256) << 20)) {
+    p.n_hsplit = 1;  // very long texts: the head sums would outgrow a modest workspace
+    p.hps = a->n_keep_heads;
+  }
   p.hpart = off;  // per-split head sums of the token-score pass
   off = align_up(off + (p.n_hsplit > 1 ? (size_t)a->B * p.n_hsplit * a->T_max * a->K_in * sizeof(float) : 0));
   p.total = off;

@@ -776,6 +776,7 @@ hipError_t launch_prep(const PrepArgs& a, int dtype, hipStream_t s) {
 constexpr int kNumCUs = 256;
 constexpr int kTile192 = 192;  // 64 text rows: 12 waves, VB = 6
 constexpr int kSplitRounds = TREVS_REL_SPLIT_ROUNDS, kSplitMinSlabs = TREVS_REL_SPLIT_MIN_SLABS;
+constexpr size_t kSplitMaxBytes = size_t(256) << 20;  // cap on the partial products
 constexpr int kStreamR32 = TREVS_STREAM_R32;
 
 size_t RelPlan::part_floats() const {
@@ -813,6 +814,10 @@ RelPlan relevance_plan(int B, int N, int M_max, int row_bytes) {
     if (want > 1) {
       p.split_slabs = (slabs + want - 1) / want;
       p.n_split = (slabs + p.split_slabs - 1) / p.split_slabs;
+      if (p.part_floats() * sizeof(float) > kSplitMaxBytes) {  // very long texts: no split
+        p.n_split = 1;
+        p.split_slabs = slabs;
+      }
     }
   }
   return p;

@@ -110,6 +110,9 @@ def test_small_grids_reserve_split_partials():
     # token score: 2 samples x 3 tiles of 64 keys split the 16 selected heads
     small = L.trevs_inllm_workspace_size(ctypes.byref(_inllm()))
     assert small >= 2 * 2 * 32 * 192 * 4        # [B, splits >= 2, T_max, K_in] floats
+    # a text so long that the split's partials would pass 256 MB runs unsplit
+    long_text = L.trevs_prellm_workspace_size(ctypes.byref(_prellm(B=1, M_max=16384)))
+    assert 0 < long_text < (64 << 20)
 
 
 @pytest.mark.parametrize("bad,code", [
