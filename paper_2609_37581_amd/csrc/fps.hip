@@ -190,6 +190,173 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Gram matrix at 256x256 tiles (N >= kGram256MinN): a workgroup of 8 waves,
+// each wave a 128x64 block (4x2 MFMA tiles), so every byte streamed from
+// L2 feeds twice the multiplies of the 128-tile form; the pass is bound by
+// the bytes in flight per CU, which stay the same (two 64 KB stages, one
+// workgroup per CU).  The fragments are read from LDS one 32-byte k-step at
+// a time to keep the accumulators, the staging ring and the fragments within
+// 256 registers.  Same swizzle, zero fill of a partial slab, super-block
+// order and outputs as gram_kernel; the mirrored tile goes through LDS in
+// four passes of 64 rows.
+// ---------------------------------------------------------------------------
+constexpr int kGram256Threads = 512;
+constexpr int kGram256MinN = 2048;
+
+template <class In>
+__global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a) {
+  constexpr int T = 256;
+  constexpr int SLAB = T * 128;                     // bytes of one operand slab
+  constexpr int VPT = SLAB / 16 / kGram256Threads;  // 4 vectors per thread per operand
+  constexpr int TP = T + 1;                         // padded row of a staged 64-row pass (floats)
+  static_assert(64 * TP * 4 <= 4 * SLAB, "mirror staging fits the operand buffers");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * SLAB];
+  uint8_t* l0 = lds;
+  uint8_t* l1 = lds + 2 * SLAB;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  const int nT = a.n_tiles;
+  const int gs = gram_super(nT), nS = (nT + gs - 1) / gs;
+  const int per_b = gram_super_pairs(nT) * gs * gs;
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = lin / per_b;
+  const int rem = lin - b * per_b, sp = rem / (gs * gs), loc = rem - sp * gs * gs;
+  int sj = 0, rs = sp;
+  while (rs >= nS - sj) {
+    rs -= nS - sj;
+    ++sj;
+  }
+  const int tj = sj * gs + loc / gs, ti = (sj + rs) * gs + loc % gs;
+  if (tj > ti || ti >= nT) return;  // the whole workgroup: no barrier has run
+  const int N = a.N, rb = a.row_bytes;
+  const int n_slabs = (rb + 127) / 128;
+  const uint8_t* zb = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
+  const int cr = tid >> 3, cc = tid & 7;
+  const uint8_t* src[2 * VPT];  // row starts (rows past N re-read row N - 1)
+#pragma unroll
+  for (int k = 0; k < VPT; ++k) {
+    const int r = cr + (kGram256Threads / 8) * k;
+    src[k] = zb + (size_t)min(tj * T + r, N - 1) * rb;
+    src[VPT + k] = zb + (size_t)min(ti * T + r, N - 1) * rb;
+  }
+  const int sdst = cr * 128 + gram_swizzle(cr, cc) * 16;  // rows 64 apart share the swizzle
+  u32x4 g[2][2 * VPT];
+  auto load = [&](int s, u32x4 (&dst)[2 * VPT]) {
+    const int off = min(s, n_slabs - 1) * 128 + cc * 16;
+    const bool in_row = off < rb;
+#pragma unroll
+    for (int k = 0; k < 2 * VPT; ++k) {
+      const u32x4 v = ldg16(src[k] + (in_row ? off : 0));
+      dst[k] = in_row ? v : zero4();
+    }
+  };
+  auto store = [&](uint8_t* st, const u32x4 (&v)[2 * VPT]) {
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) {
+      *reinterpret_cast<u32x4*>(st + sdst + k * (kGram256Threads / 8) * 128) = v[k];
+      *reinterpret_cast<u32x4*>(st + SLAB + sdst + k * (kGram256Threads / 8) * 128) = v[VPT + k];
+    }
+  };
+  const int wj = wave >> 2, wi = wave & 3;  // rows wj*128.., columns wi*64.. of the tile
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
+  auto compute = [&](const uint8_t* st) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {  // k-step q: chunk 4*half + q of each row
+      u32x4 fa[4][1], fb[2][1];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int row = wj * 128 + m * 32 + col;
+        fa[m][0] = *reinterpret_cast<const u32x4*>(st + row * 128 + gram_swizzle(row, 4 * half + q) * 16);
+      }
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        const int row = wi * 64 + n * 32 + col;
+        fb[n][0] = *reinterpret_cast<const u32x4*>(st + SLAB + row * 128 + gram_swizzle(row, 4 * half + q) * 16);
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 2; ++n) acc[m][n] = mfma_frag(fa[m], fb[n], acc[m][n], In{});
+    }
+  };
+  load(0, g[0]);
+  load(1, g[1]);
+  const int n_iter = (n_slabs + 1) / 2;
+  for (int it = 0; it < n_iter; ++it) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int s = 2 * it + c;
+      uint8_t* st = c ? l1 : l0;
+      // buffer c was last read at step s - 2, before every wave passed the
+      // barrier of step s - 1
+      store(st, g[c]);
+      load(s + 2, g[c]);
+      __syncthreads();
+      if (s < n_slabs) compute(st);
+    }
+  }
+  // register r of block (m, n) is row wj*128 + m*32 + mfma_row(r), column
+  // wi*64 + n*32 + col of the tile
+  float* gbm = a.G + (size_t)b * N * N;
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int n = 0; n < 2; ++n) {
+      const int i = ti * T + wi * 64 + n * 32 + col;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = tj * T + wj * 128 + m * 32 + mfma_row(r, half);
+        if (i < N && j < N) gbm[(size_t)j * N + i] = acc[m][n][r];
+      }
+    }
+  if (tj == ti) {  // the diagonal tile holds ||z_i||^2
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int jl = wj * 128 + m * 32 + mfma_row(r, half), il = wi * 64 + n * 32 + col;
+          const int i = ti * T + il;
+          if (jl == il && i < N)
+            a.inv_norm[(size_t)b * N + i] = 1.f / fmaxf(sqrtf(fmaxf(acc[m][n][r], 0.f)), 1e-12f);
+        }
+    return;
+  }
+  // the mirrored tile G[i, j], 64 tile rows jl at a time: the two waves'
+  // 32-row blocks of the pass stage tile[jl - 64p][il], then every thread
+  // writes rows il with consecutive jl per lane
+  float* tile = reinterpret_cast<float*>(lds);
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    __syncthreads();  // the operand slabs, or the previous pass, are no longer read
+    if (wj == p / 2) {
+#pragma unroll
+      for (int mm = 0; mm < 2; ++mm) {
+        const int m = 2 * (p % 2) + mm;
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            tile[(mm * 32 + mfma_row(r, half)) * TP + wi * 64 + n * 32 + col] = acc[m][n][r];
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < T * 64; e += kGram256Threads) {
+      const int il = e >> 6, jl = e & 63;
+      const int i = ti * T + il, j = tj * T + 64 * p + jl;
+      if (i < N && j < N) gbm[(size_t)i * N + j] = tile[jl * TP + il];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Initial distances: for every token i, 1 - max over the pivots j of
 // cos(z_i, z_j) = G_ij / (||z_i|| ||z_j||), with the inverse norms the Gram
 // pass wrote.  One thread per token; the pivot loop is unrolled so that
@@ -304,11 +471,21 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hipStream_t s) {
-  const dim3 ggrid(B * gram_super_pairs(g.n_tiles) * gram_super(g.n_tiles) * gram_super(g.n_tiles));
-  if (dtype == 1)
-    hipLaunchKernelGGL(gram_kernel<BF16>, ggrid, dim3(kGramThreads), 0, s, g);
-  else
-    hipLaunchKernelGGL(gram_kernel<F32>, ggrid, dim3(kGramThreads), 0, s, g);
+  if (g.N >= kGram256MinN) {
+    GramArgs g2 = g;
+    g2.n_tiles = (g.N + 255) / 256;
+    const dim3 ggrid(B * gram_super_pairs(g2.n_tiles) * gram_super(g2.n_tiles) * gram_super(g2.n_tiles));
+    if (dtype == 1)
+      hipLaunchKernelGGL(gram256_kernel<BF16>, ggrid, dim3(kGram256Threads), 0, s, g2);
+    else
+      hipLaunchKernelGGL(gram256_kernel<F32>, ggrid, dim3(kGram256Threads), 0, s, g2);
+  } else {
+    const dim3 ggrid(B * gram_super_pairs(g.n_tiles) * gram_super(g.n_tiles) * gram_super(g.n_tiles));
+    if (dtype == 1)
+      hipLaunchKernelGGL(gram_kernel<BF16>, ggrid, dim3(kGramThreads), 0, s, g);
+    else
+      hipLaunchKernelGGL(gram_kernel<F32>, ggrid, dim3(kGramThreads), 0, s, g);
+  }
   hipLaunchKernelGGL(fps_init_kernel, dim3((f.N + kFpsInitThreads - 1) / kFpsInitThreads, B),
                      dim3(kFpsInitThreads), 0, s, f);
   const int E = select_e(f.N);

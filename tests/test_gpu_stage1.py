@@ -292,6 +292,11 @@ FPS_CASES = {
         text_len=("uniform", 1, 40)), 9),
     "tie-stress-bf16": (WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, tie_stress=True), 30),
     "one-pivot-bf16": (WORKLOADS["llava15-b64-bf16"].with_(B=1, K1=20), 19),
+    # N >= 2048: the 256-row Gram tiles (ragged N, a partial 128-byte slab,
+    # two super-blocks a side; fp32)
+    "gram256-ragged-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=2, N=2500, d=520, K1=300, n_sal=8, n_qm=10), 100),
+    "gram256-f32": (WORKLOADS["llava15-b1-f32"].with_(N=2100, d=256, K1=200), 60),
 }
 
 
