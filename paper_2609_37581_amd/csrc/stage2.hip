@@ -288,6 +288,9 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
 // recomputed on the matrix cores (operand A = text rows, operand B = key
 // rows), turned into attention and summed over heads in-lane.  Then max over
 // the valid text rows, across waves via LDS, and divide by |H*| (Eq. (9)).
+// With a head split (small grids) workgroup (tile, split) sums only its hps
+// selected heads and writes the sums per (valid text row, token);
+// t2v_score_merge_kernel finishes Eq. (9).
 // ---------------------------------------------------------------------------
 constexpr int kMaxHeads = 256;
 
