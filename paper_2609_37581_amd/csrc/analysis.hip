@@ -191,11 +191,21 @@ __global__ __launch_bounds__(kSensThreads) void sensitivity_kernel(SensitivityAr
   const int h = blockIdx.x, b = blockIdx.y;
   const size_t base = ((size_t)b * a.H_q + h) * a.K_in;
   double d = 0.0, n0 = 0.0, n1 = 0.0;
-  for (int i = tid; i < a.K_in; i += kSensThreads) {
-    const double x = a.profile[0][base + i], y = a.profile[1][base + i];
-    d = fma(x, y, d);
-    n0 = fma(x, x, n0);
-    n1 = fma(y, y, n1);
+  for (int i0 = tid; i0 < a.K_in; i0 += 8 * kSensThreads) {  // 16 loads in flight
+    float x[8], y[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = min(i0 + k * kSensThreads, a.K_in - 1);
+      x[k] = a.profile[0][base + i];
+      y[k] = a.profile[1][base + i];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (i0 + k * kSensThreads < a.K_in) {
+        d = fma((double)x[k], (double)y[k], d);
+        n0 = fma((double)x[k], (double)x[k], n0);
+        n1 = fma((double)y[k], (double)y[k], n1);
+      }
   }
   d = wave_sum_f64(d);
   n0 = wave_sum_f64(n0);

@@ -682,25 +682,35 @@ __global__ __launch_bounds__(kSelThreads) void fuse_topk_kernel(SelArgs a) {
   const float* st_p = a.rel + (size_t)b * N;
   const float med_v = a.stats[4 * b + 0], mad_v = a.stats[4 * b + 1];
   const float med_t = a.stats[4 * b + 2], mad_t = a.stats[4 * b + 3];
-  if (a.norm_stats && tid < 4) a.norm_stats[4 * b + tid] = a.stats[4 * b + tid];
   // one workgroup holds a whole sample, so the per-token arithmetic is kept
   // to multiplies: the branch weight, 1/(MAD + eps) and 1/tau are folded into
   // one factor per branch, and the square root is the hardware one (a few
   // ulp from the exactly rounded expression of Eq. (6)-(7))
   const float cv = a.wv / ((mad_v + a.eps) * a.tau_v);
   const float ct = a.wt / ((mad_t + a.eps) * a.tau_t);
+  // every load before the first store: a store to score_out may alias the
+  // inputs as far as the compiler knows, which would serialise the loads
+  float sv[E], st[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = min(e * kSelThreads + tid, N - 1);
+    sv[e] = sv_p[i];
+    st[e] = st_p[i];
+  }
   float sc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const int i = e * kSelThreads + tid;
-    const bool ok = i < N;
-    const float sv = ok ? sv_p[i] : 0.f, st = ok ? st_p[i] : 0.f;
-    const float dv = fmaxf(sv - med_v, 0.f), dt = fmaxf(st - med_t, 0.f);
+    const float dv = fmaxf(sv[e] - med_v, 0.f), dt = fmaxf(st[e] - med_t, 0.f);
     const float av = dv > 0.f ? dv * cv : 0.f;  // clamped tokens stay exactly 0
     const float bt = dt > 0.f ? dt * ct : 0.f;
-    sc[e] = fmaxf(av, bt) + a.lam * __builtin_amdgcn_sqrtf(av * bt);
-    if (a.score_out && ok) a.score_out[(size_t)b * N + i] = sc[e];
+    sc[e] = e * kSelThreads + tid < N ? fmaxf(av, bt) + a.lam * __builtin_amdgcn_sqrtf(av * bt) : 0.f;
   }
+  if (a.score_out) {
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (e * kSelThreads + tid < N) a.score_out[(size_t)b * N + e * kSelThreads + tid] = sc[e];
+  }
+  if (a.norm_stats && tid < 4) a.norm_stats[4 * b + tid] = a.stats[4 * b + tid];
   block_topk_write<E>(sc, N, a.K, a.kept_idx + (size_t)b * a.K, sh);
 }
 

@@ -225,15 +225,23 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
     const size_t row = ((size_t)b * a.H_q + h) * a.T_max + q;
     const float4* pp = a.part + row * a.n_split;
     const size_t lrow = ((size_t)b * a.H_q + h) * a.T_pad + q;
+    // the splits' partials 8 at a time, every load issued before the merge
     float m = -INFINITY, l = 0.f, l2 = 0.f;
-    for (int s = 0; s < a.n_split; ++s) {
-      const float4 p = pp[s];
-      const float mn = fmaxf(m, p.x);
-      if (mn == -INFINITY) continue;
-      const float c1 = fast_exp2(m - mn), c2 = fast_exp2(p.x - mn);
-      l = l * c1 + p.y * c2;
-      l2 = l2 * c1 * c1 + p.z * c2 * c2;
-      m = mn;
+    for (int s0 = 0; s0 < a.n_split; s0 += 8) {
+      float4 pv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) pv[k] = pp[min(s0 + k, a.n_split - 1)];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float4 p = pv[k];
+        const float mn = fmaxf(m, p.x);
+        if (s0 + k < a.n_split && mn > -INFINITY) {
+          const float c1 = fast_exp2(m - mn), c2 = fast_exp2(p.x - mn);
+          l = l * c1 + p.y * c2;
+          l2 = l2 * c1 * c1 + p.z * c2 * c2;
+          m = mn;
+        }
+      }
     }
     float lse2 = m + log2f(l);
     if (a.lse_rest || a.part_rest) {
@@ -241,12 +249,19 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
       if (a.part_rest) {
         const float4* pr = a.part_rest + row * a.n_split;
         float mr = -INFINITY, lr = 0.f;
-        for (int s = 0; s < a.n_split; ++s) {
-          const float4 p = pr[s];
-          const float mn = fmaxf(mr, p.x);
-          if (mn == -INFINITY) continue;
-          lr = lr * fast_exp2(mr - mn) + p.y * fast_exp2(p.x - mn);
-          mr = mn;
+        for (int s0 = 0; s0 < a.n_split; s0 += 8) {
+          float4 pv[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) pv[k] = pr[min(s0 + k, a.n_split - 1)];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const float4 p = pv[k];
+            const float mn = fmaxf(mr, p.x);
+            if (s0 + k < a.n_split && mn > -INFINITY) {
+              lr = lr * fast_exp2(mr - mn) + p.y * fast_exp2(p.x - mn);
+              mr = mn;
+            }
+          }
         }
         r2 = mr + log2f(lr);
       } else {
