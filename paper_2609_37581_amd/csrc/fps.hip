@@ -412,20 +412,28 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
   const int32_t* piv = a.pivots + (size_t)b * K_r;
   const float* gb = a.G + (size_t)b * N * N;
   auto valid = [&](int e) { return e * kSelThreads + tid < N; };
+  // pivot membership: every thread marks its share of the pivot list in an
+  // LDS bitmap, then reads the bits of its own elements
+  __shared__ uint32_t pivbits[kMaxE * kSelThreads / 32];
+  for (int w = tid; w < (N + 31) / 32; w += kSelThreads) pivbits[w] = 0u;
   float dist[E], iz[E];
-  uint32_t sel = 0u;  // bit e: element e is selected (a pivot or a pick)
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int i = min(e * kSelThreads + tid, N - 1);
     dist[e] = a.dist[(size_t)b * N + i];
     iz[e] = a.inv_norm[(size_t)b * N + i];
-    // pivot membership by binary search in the ascending pivot list
-    int lo = 0, hi = K_r;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (piv[mid] < i) lo = mid + 1; else hi = mid;
-    }
-    if (valid(e) && lo < K_r && piv[lo] == i) sel |= 1u << e;
+  }
+  __syncthreads();
+  for (int p = tid; p < K_r; p += kSelThreads) {
+    const int j = min(max(piv[p], 0), N - 1);
+    atomicOr(&pivbits[j >> 5], 1u << (j & 31));
+  }
+  __syncthreads();
+  uint32_t sel = 0u;  // bit e: element e is selected (a pivot or a pick)
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = e * kSelThreads + tid;
+    if (valid(e) && ((pivbits[i >> 5] >> (i & 31)) & 1u)) sel |= 1u << e;
   }
   for (int t = 0; t < a.K_d; ++t) {
     float v = -INFINITY;
