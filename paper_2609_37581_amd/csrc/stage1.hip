@@ -285,15 +285,19 @@ __global__ __launch_bounds__(64 * NW) void relevance_kernel(RelArgs a) {
     // ---- epilogue of this text chunk: sum_j max(t_j.z_i / ||t_j||, 0)^2
     const float* itn = a.inv_tnorm + (size_t)b * a.M_max;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+    for (int mb = 0; mb < MB; ++mb) {
+      float w[16];  // every norm load before the first use
+#pragma unroll
+      for (int r = 0; r < 16; ++r) w[r] = itn[min(j0 + mb * 32 + mfma_row(r, half), a.M_max - 1)];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = j0 + mb * 32 + mfma_row(r, half);
         if (j < Mb) {
-          const float c = fmaxf(acc[mb][r] * itn[j], 0.f);
+          const float c = fmaxf(acc[mb][r] * w[r], 0.f);
           rsum = fmaf(c, c, rsum);
         }
       }
+    }
     __syncthreads();  // the next chunk refills both LDS buffers
   }
   const float zz = zsq + __shfl_xor(zsq, 32, 64);
@@ -747,10 +751,10 @@ __global__ __launch_bounds__(kSelThreads) void topk_kernel(const float* scores, 
   const float* p = scores + (size_t)b * N;
   float sc[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = e * kSelThreads + tid;
-    sc[e] = i < N ? p[i] : 0.f;
-  }
+  for (int e = 0; e < E; ++e) sc[e] = p[min(e * kSelThreads + tid, N - 1)];  // unconditional loads
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (e * kSelThreads + tid >= N) sc[e] = 0.f;
   block_topk_write<E>(sc, N, K, out + (size_t)b * K, sh);
 }
 
