@@ -172,9 +172,8 @@ __device__ __forceinline__ int wave_incl_scan(int v, int /*lane*/) {
 
 // Order-preserving map from fp32 to uint32 (-0 taken as +0).
 __device__ __forceinline__ uint32_t f2key(float f) {
-  uint32_t u = __float_as_uint(f);
-  if (u == 0x80000000u) u = 0u;
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  const uint32_t u = __float_as_uint(f + 0.0f);  // -0 + +0 is +0: both zeros share one key
+  return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
 }
 __device__ __forceinline__ float key2f(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);

@@ -89,30 +89,47 @@ __device__ __forceinline__ void wave0_find_bin(int krem, SelectShared& sh) {
   __syncthreads();
 }
 
-// Histogram pass over this thread's elements: keys equal to the set minimum
+// A copy of v that the compiler cannot see through, so that compares on it are
+// redone where they are used instead of being kept live (as one 64-bit lane
+// mask per element) across a whole selection.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// Number of this thread's valid elements: element e is valid iff e < rounds.
+template <int E>
+__device__ __forceinline__ int thread_rounds(int N) {
+  const int t = (int)threadIdx.x;
+  return N > t ? min(E, (N - t + kSelThreads - 1) / kSelThreads) : 0;
+}
+
+// Histogram pass over this thread's keys: keys equal to the set minimum
 // `kmin` (often a large tie, e.g. exact zeros) are counted with one ballot per
-// wave and added once; every other key adds one to its digit's bin.
-template <int E, class KeyF, class Match>
-__device__ __forceinline__ void hist_pass(KeyF keyf, Match match, int N, uint32_t kmin, int shift,
-                                          uint32_t dmask, SelectShared& sh) {
+// wave and added once; every other key adds one to its digit's bin (bits
+// [shift, shift + db) of the key).
+template <int E, class Match>
+__device__ __forceinline__ void hist_pass(const uint32_t (&k)[E], int nv, Match match, uint32_t kmin,
+                                          int shift, int db, SelectShared& sh) {
   const int lane = threadIdx.x & (kWave - 1);
-  int nmin = 0;
+  nv = opaque(nv);
+  int nmin = 0;  // per lane, summed over the wave once
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const uint32_t k = keyf(e);
-    const bool act = e * kSelThreads + (int)threadIdx.x < N && match(k);
-    const bool is_min = act && k == kmin;
-    nmin += __popcll(__ballot(is_min));
-    if (act && !is_min) atomicAdd(&sh.hist[(k >> shift) & dmask], 1u);
+    const bool act = e < nv && match(k[e]);
+    nmin += (act && k[e] == kmin) ? 1 : 0;
+    if (act && k[e] != kmin) atomicAdd(&sh.hist[__builtin_amdgcn_ubfe(k[e], shift, db)], 1u);
   }
-  if (lane == 0 && nmin) atomicAdd(&sh.hist[(kmin >> shift) & dmask], (uint32_t)nmin);
+  nmin = wave_reduce_bits(nmin, 0, [](int x, int y) { return x + y; });
+  if (lane == 0 && nmin) atomicAdd(&sh.hist[__builtin_amdgcn_ubfe(kmin, shift, db)], (uint32_t)nmin);
 }
 
 // Exact rank selection on uint32 keys.  keyf(e) yields the key of this
-// thread's element e (recomputed on demand, not held).  Returns the key of
-// ascending 0-based rank `rank` among the N valid keys, with the number of
-// keys strictly below it (less) and equal to it (eq).  If have_range, kmin and
-// kmax are the minimum and maximum key (else they are computed).
+// thread's element e; it is evaluated once per element and the keys are held
+// in registers.  Returns the key of ascending 0-based rank `rank` among the N
+// valid keys, with the number of keys strictly below it (less) and equal to it
+// (eq).  If have_range, kmin and kmax are the minimum and maximum key (else
+// they are computed).
 //   1. the bits above the highest bit where min and max differ are common;
 //   2. one pass over all elements on the next (up to) 11 bits;
 //   3. the keys in the chosen bin are appended to LDS (if they fit) and the
@@ -123,16 +140,18 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
                              SelectShared& sh, bool have_range = false, uint32_t kmin = 0u,
                              uint32_t kmax = 0u) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  auto valid = [&](int e) { return e * kSelThreads + tid < N; };
+  const int nv = thread_rounds<E>(N);
+  uint32_t k[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) k[e] = keyf(e);
   uint32_t a = kmin, z = kmax;
   if (!have_range) {
     uint32_t mn = 0xffffffffu, mx = 0u;
 #pragma unroll
     for (int e = 0; e < E; ++e)
-      if (valid(e)) {
-        const uint32_t k = keyf(e);
-        mn = min(mn, k);
-        mx = max(mx, k);
+      if (e < nv) {
+        mn = min(mn, k[e]);
+        mx = max(mx, k[e]);
       }
     mn = wave_min_u32(mn);
     mx = wave_max_u32(mx);
@@ -160,7 +179,6 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
   int nb = 32 - __clz(diff);
   uint32_t prefix = (uint32_t)(((uint64_t)a >> nb) << nb);
   int krem = rank;
-  auto under_prefix = [&](uint32_t k) { return ((uint64_t)k >> nb) == ((uint64_t)prefix >> nb); };
 
   // ---- first pass: every element shares the prefix above bit nb
   {
@@ -169,7 +187,7 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
     for (int i = tid; i < nbins; i += kSelThreads) sh.hist[i] = 0u;
     if (tid == 0) sh.total = 0;
     __syncthreads();
-    hist_pass<E>(keyf, [](uint32_t) { return true; }, N, a, shift, (1u << db) - 1u, sh);
+    hist_pass<E>(k, nv, [](uint32_t) { return true; }, a, shift, db, sh);
     __syncthreads();
     block_find_bin(nbins, krem, sh);
     prefix |= sh.res_digit << shift;
@@ -182,38 +200,40 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
     res = prefix;
     return;
   }
+  // from here on nb <= 31: keys under the prefix share their bits above nb
+  const auto under_prefix = [&](uint32_t key) { return (key >> nb) == (prefix >> nb); };
   const int ncand = eq;
   if (ncand <= kCandCap) {
     // ---- append the candidates (keys sharing the prefix above bit nb);
     // their order does not matter for a rank selection.  One LDS atomic per
     // wave reserves room for all of the wave's candidates.
     int wn = 0;
+    const int nv1 = opaque(nv);
 #pragma unroll
-    for (int e = 0; e < E; ++e) wn += __popcll(__ballot(valid(e) && under_prefix(keyf(e))));
+    for (int e = 0; e < E; ++e) wn += __popcll(__ballot(e < nv1 && under_prefix(k[e])));
     int wbase = 0;
     if (lane == 0 && wn) wbase = atomicAdd(&sh.total, wn);
     wbase = __builtin_amdgcn_readfirstlane(wbase);
+    const int nv2 = opaque(nv);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const uint32_t k = keyf(e);
-      const bool m = valid(e) && under_prefix(k);
+      const bool m = e < nv2 && under_prefix(k[e]);
       const unsigned long long bal = __ballot(m);
       const int pos = wbase + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-      if (m && pos < kCandCap) sh.cand[pos] = k;
+      if (m && pos < kCandCap) sh.cand[pos] = k[e];
       wbase += __popcll(bal);
     }
     __syncthreads();
     const int rounds = (ncand + kSelThreads - 1) / kSelThreads;
     while (nb > 0) {
       const int db = min(kLaterBits, nb), shift = nb - db;
-      const uint32_t dmask = (1u << db) - 1u;
       if (tid < (1 << kLaterBits)) sh.hist[tid] = 0u;
       __syncthreads();
       for (int r = 0; r < rounds; ++r) {
         const int c = r * kSelThreads + tid;
-        const uint32_t k = c < ncand ? sh.cand[c] : 0u;
-        if (c < ncand && under_prefix(k)) atomicAdd(&sh.hist[(k >> shift) & dmask], 1u);
+        const uint32_t key = c < ncand ? sh.cand[c] : 0u;
+        if (c < ncand && under_prefix(key)) atomicAdd(&sh.hist[__builtin_amdgcn_ubfe(key, shift, db)], 1u);
       }
       __syncthreads();
       wave0_find_bin(krem, sh);
@@ -230,7 +250,7 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
       const int db = min(kLaterBits, nb), shift = nb - db;
       if (tid < (1 << kLaterBits)) sh.hist[tid] = 0u;
       __syncthreads();
-      hist_pass<E>(keyf, under_prefix, N, a, shift, (1u << db) - 1u, sh);
+      hist_pass<E>(k, nv, under_prefix, a, shift, db, sh);
       __syncthreads();
       wave0_find_bin(krem, sh);
       prefix |= sh.res_digit << shift;
@@ -272,7 +292,8 @@ __device__ __forceinline__ void wcnt_scan(int n, SelectShared& sh) {
 template <int E, class KeyF>
 __device__ uint32_t block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  auto valid = [&](int e) { return e * kSelThreads + tid < N; };
+  const int nv = thread_rounds<E>(N);
+  auto valid = [&](int e) { return e < nv; };
   if (K <= 0) return 0u;
   if (K >= N) {
     uint32_t all = 0u;
@@ -280,9 +301,12 @@ __device__ uint32_t block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
     for (int e = 0; e < E; ++e) all |= valid(e) ? (1u << e) : 0u;
     return all;
   }
+  uint32_t key[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) key[e] = keyf(e);
   uint32_t thr;
   int less, eq;
-  block_select<E>(keyf, N, N - K, thr, less, eq, sh);
+  block_select<E>([&](int e) { return key[e]; }, N, N - K, thr, less, eq, sh);
   const int need_eq = K - (N - less - eq);
   auto lanes_below = [&](unsigned long long bal) {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
@@ -290,7 +314,7 @@ __device__ uint32_t block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
   };
   // rank of every tie among the ties, in index order (ballots are recomputed
   // after each scan rather than held)
-  auto is_eq = [&](int e) { return valid(e) && keyf(e) == thr; };
+  auto is_eq = [&](int e) { return valid(e) && key[e] == thr; };
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const unsigned long long bal = __ballot(is_eq(e));
@@ -302,7 +326,7 @@ __device__ uint32_t block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
   for (int e = 0; e < E; ++e) {
     const bool eqe = is_eq(e);
     const int eq_rank = sh.wcnt[e * kSelWaves + wave] + lanes_below(__ballot(eqe));
-    const bool keep = valid(e) && (keyf(e) > thr || (eqe && eq_rank < need_eq));
+    const bool keep = valid(e) && (key[e] > thr || (eqe && eq_rank < need_eq));
     keep_mask |= keep ? (1u << e) : 0u;
   }
   __syncthreads();  // sh.wcnt is rewritten by the caller's next step
@@ -343,7 +367,8 @@ template <int E>
 __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* out,
                                  SelectShared& sh) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  auto valid = [&](int e) { return e * kSelThreads + tid < N; };
+  const int nv = thread_rounds<E>(N);
+  auto valid = [&](int e) { return e < nv; };
   if (K <= 0) return;
   if (K >= N) {
 #pragma unroll
@@ -351,10 +376,12 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
       if (valid(e)) out[e * kSelThreads + tid] = e * kSelThreads + tid;
     return;
   }
-  auto keyf = [&](int e) { return f2key(sc[e]); };
+  uint32_t key[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) key[e] = f2key(sc[e]);
   uint32_t thr;
   int less, eq;
-  block_select<E>(keyf, N, N - K, thr, less, eq, sh);
+  block_select<E>([&](int e) { return key[e]; }, N, N - K, thr, less, eq, sh);
   const int need = K - (N - less - eq);  // ties kept, lowest index first
   auto lanes_below = [&](unsigned long long bal) {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
@@ -362,7 +389,7 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
   };
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const uint32_t k = keyf(e);
+    const uint32_t k = key[e];
     const unsigned long long ba = __ballot(valid(e) && k > thr);
     const unsigned long long bt = __ballot(valid(e) && k == thr);
     if (lane == 0) sh.wcnt[e * kSelWaves + wave] = __popcll(ba) | (__popcll(bt) << 16);
@@ -370,7 +397,7 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
   wcnt_scan(E * kSelWaves, sh);
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const uint32_t k = keyf(e);
+    const uint32_t k = key[e];
     const bool above = valid(e) && k > thr, tie = valid(e) && k == thr;
     const unsigned long long ba = __ballot(above);
     const unsigned long long bt = __ballot(tie);
