@@ -44,6 +44,30 @@ def test_topk_signs_zeros_and_all_equal():
         check(two, k)
 
 
+def test_topk_crowded_first_digit_bin():
+    """More than 4096 keys share the threshold's first 11-bit digit, so the
+    selection resolves the remaining bits over all elements instead of an LDS
+    candidate list; once with the crowded bin above the minimum, once with
+    the minimum itself in it (its ties counted by ballot)."""
+    rng = np.random.default_rng(11)
+    for N in (16384, 32768):
+        above = rng.random((2, N)).astype(np.float32)
+        crowd = rng.random((2, N)) < 0.4
+        above[crowd] = np.float32(2.0) + rng.integers(0, 3, size=crowd.sum()).astype(np.float32) * np.float32(2.0 ** -22)
+        above[:, :50] = np.float32(7.0)
+        for k in (60, N // 3, N // 2):
+            print(f"[topk crowded] N={N} K={k}", flush=True)
+            check(above, k)
+        low = (np.float32(0.1) + rng.random((2, N)).astype(np.float32)).astype(np.float32)
+        at_min = rng.random((2, N)) < 0.5
+        low[at_min] = np.float32(0.1)
+        near = rng.random((2, N)) < 0.05
+        low[near & ~at_min] = np.float32(0.1) + np.float32(2.0 ** -26)
+        for k in (N - 10, N - N // 3, N // 2):
+            print(f"[topk crowded min] N={N} K={k}", flush=True)
+            check(low, k)
+
+
 def test_topk_batch_of_many_rows():
     rng = np.random.default_rng(3)
     s = rng.standard_normal((257, 300)).astype(np.float32)
