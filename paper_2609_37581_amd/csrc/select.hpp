@@ -104,19 +104,19 @@ __device__ __forceinline__ int thread_rounds(int N) {
   return N > t ? min(E, (N - t + kSelThreads - 1) / kSelThreads) : 0;
 }
 
-// Histogram pass over this thread's keys: keys equal to the set minimum
+// Histogram pass over this thread's keys (all E of them: unused slots hold
+// the minimum key, see block_select): keys equal to the set minimum
 // `kmin` (often a large tie, e.g. exact zeros) are counted with one ballot per
 // wave and added once; every other key adds one to its digit's bin (bits
 // [shift, shift + db) of the key).
 template <int E, class Match>
-__device__ __forceinline__ void hist_pass(const uint32_t (&k)[E], int nv, Match match, uint32_t kmin,
+__device__ __forceinline__ void hist_pass(const uint32_t (&k)[E], Match match, uint32_t kmin,
                                           int shift, int db, SelectShared& sh) {
   const int lane = threadIdx.x & (kWave - 1);
-  nv = opaque(nv);
   int nmin = 0;  // per lane, summed over the wave once
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const bool act = e < nv && match(k[e]);
+    const bool act = match(k[e]);
     nmin += (act && k[e] == kmin) ? 1 : 0;
     if (act && k[e] != kmin) atomicAdd(&sh.hist[__builtin_amdgcn_ubfe(k[e], shift, db)], 1u);
   }
@@ -128,8 +128,11 @@ __device__ __forceinline__ void hist_pass(const uint32_t (&k)[E], int nv, Match 
 // thread's element e; it is evaluated once per element and the keys are held
 // in registers.  Returns the key of ascending 0-based rank `rank` among the N
 // valid keys, with the number of keys strictly below it (less) and equal to it
-// (eq).  If have_range, kmin and kmax are the minimum and maximum key (else
-// they are computed).
+// (eq).  If have_range, kmin and kmax are the minimum and maximum key, or
+// bounds of them (else they are computed).  N <= E * 1024.
+//   0. the E * 1024 - N unused slots take the key kmin: they sort first, so
+//      rank r among the valid keys is rank r + (E * 1024 - N) among all
+//      slots, and no pass tests validity;
 //   1. the bits above the highest bit where min and max differ are common;
 //   2. one pass over all elements on the next (up to) 11 bits;
 //   3. the keys in the chosen bin are appended to LDS (if they fit) and the
@@ -176,9 +179,13 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
     eq = N;
     return;
   }
+  const int n_unused = E * kSelThreads - N;
+  const int nv_sub = opaque(nv);
+#pragma unroll
+  for (int e = 0; e < E; ++e) k[e] = e < nv_sub ? k[e] : a;
   int nb = 32 - __clz(diff);
   uint32_t prefix = (uint32_t)(((uint64_t)a >> nb) << nb);
-  int krem = rank;
+  int krem = rank + n_unused;
 
   // ---- first pass: every element shares the prefix above bit nb
   {
@@ -187,7 +194,7 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
     for (int i = tid; i < nbins; i += kSelThreads) sh.hist[i] = 0u;
     if (tid == 0) sh.total = 0;
     __syncthreads();
-    hist_pass<E>(k, nv, [](uint32_t) { return true; }, a, shift, db, sh);
+    hist_pass<E>(k, [](uint32_t) { return true; }, a, shift, db, sh);
     __syncthreads();
     block_find_bin(nbins, krem, sh);
     prefix |= sh.res_digit << shift;
@@ -196,28 +203,24 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
     nb = shift;
     eq = (int)sh.res_count;
   }
-  if (nb == 0) {
-    res = prefix;
-    return;
-  }
   // from here on nb <= 31: keys under the prefix share their bits above nb
   const auto under_prefix = [&](uint32_t key) { return (key >> nb) == (prefix >> nb); };
   const int ncand = eq;
-  if (ncand <= kCandCap) {
+  if (nb == 0) {
+    // the first digit resolved every bit
+  } else if (ncand <= kCandCap) {
     // ---- append the candidates (keys sharing the prefix above bit nb);
     // their order does not matter for a rank selection.  One LDS atomic per
     // wave reserves room for all of the wave's candidates.
     int wn = 0;
-    const int nv1 = opaque(nv);
 #pragma unroll
-    for (int e = 0; e < E; ++e) wn += __popcll(__ballot(e < nv1 && under_prefix(k[e])));
+    for (int e = 0; e < E; ++e) wn += __popcll(__ballot(under_prefix(k[e])));
     int wbase = 0;
     if (lane == 0 && wn) wbase = atomicAdd(&sh.total, wn);
     wbase = __builtin_amdgcn_readfirstlane(wbase);
-    const int nv2 = opaque(nv);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const bool m = e < nv2 && under_prefix(k[e]);
+      const bool m = under_prefix(k[e]);
       const unsigned long long bal = __ballot(m);
       const int pos = wbase + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
@@ -250,7 +253,7 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
       const int db = min(kLaterBits, nb), shift = nb - db;
       if (tid < (1 << kLaterBits)) sh.hist[tid] = 0u;
       __syncthreads();
-      hist_pass<E>(k, nv, under_prefix, a, shift, db, sh);
+      hist_pass<E>(k, under_prefix, a, shift, db, sh);
       __syncthreads();
       wave0_find_bin(krem, sh);
       prefix |= sh.res_digit << shift;
@@ -262,6 +265,11 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
     }
   }
   res = prefix;
+  // the unused slots hold the key a: below res, or tied with it
+  if (res == a)
+    eq -= n_unused;
+  else
+    less -= n_unused;
 }
 
 // Exclusive prefix sums of sh.wcnt[0, n) in place (n <= kMaxE * kSelWaves),
@@ -395,6 +403,11 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
     if (lane == 0) sh.wcnt[e * kSelWaves + wave] = __popcll(ba) | (__popcll(bt) << 16);
   }
   wcnt_scan(E * kSelWaves, sh);
+  // the output base lives in a VGPR pair: held in SGPRs through the
+  // selection it was spilled and re-read for every store
+  uint64_t obase = (uint64_t)(uintptr_t)out;
+  asm volatile("" : "+v"(obase));
+  int32_t* const o = (int32_t*)(uintptr_t)obase;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const uint32_t k = key[e];
@@ -406,7 +419,7 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
     const int nt = (base >> 16) + lanes_below(bt);     // ties before this element
     if (above || (tie && nt < need)) {
       const int pos = na + min(nt, need);
-      if (pos < K) out[pos] = e * kSelThreads + tid;  // exactly K kept; the bound guards memory
+      if (pos < K) o[pos] = e * kSelThreads + tid;  // exactly K kept; the bound guards memory
     }
   }
 }
