@@ -371,9 +371,11 @@ __device__ void block_write_mask(uint32_t mask, int K, int32_t* out, SelectShare
 // above(i) and ties(i) count the elements before i (in index order) above the
 // threshold and equal to it, and need is how many ties are kept.  The two
 // counts travel packed in one int (low and high 16 bits; N <= 32768).
+// have_range, kmin, kmax: bounds of the keys, as for block_select.
 template <int E>
 __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* out,
-                                 SelectShared& sh) {
+                                 SelectShared& sh, bool have_range = false, uint32_t kmin = 0u,
+                                 uint32_t kmax = 0u) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int nv = thread_rounds<E>(N);
   auto valid = [&](int e) { return e < nv; };
@@ -389,7 +391,7 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
   for (int e = 0; e < E; ++e) key[e] = f2key(sc[e]);
   uint32_t thr;
   int less, eq;
-  block_select<E>([&](int e) { return key[e]; }, N, N - K, thr, less, eq, sh);
+  block_select<E>([&](int e) { return key[e]; }, N, N - K, thr, less, eq, sh, have_range, kmin, kmax);
   const int need = K - (N - less - eq);  // ties kept, lowest index first
   auto lanes_below = [&](unsigned long long bal) {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),

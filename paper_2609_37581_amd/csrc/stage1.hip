@@ -715,7 +715,11 @@ __global__ __launch_bounds__(kSelThreads) void fuse_topk_kernel(SelArgs a) {
       if (e * kSelThreads + tid < N) a.score_out[(size_t)b * N + e * kSelThreads + tid] = sc[e];
   }
   if (a.norm_stats && tid < 4) a.norm_stats[4 * b + tid] = a.stats[4 * b + tid];
-  block_topk_write<E>(sc, N, a.K, a.kept_idx + (size_t)b * a.K, sh);
+  // with lam >= 0 every score is a sum of non-negative terms, so the keys lie
+  // in [key(+0), 0xffffffff] and the selection needs no min/max reduction
+  // (the bound spans the same 31 bits as the exact range once any score is 0)
+  block_topk_write<E>(sc, N, a.K, a.kept_idx + (size_t)b * a.K, sh, a.lam >= 0.f, f2key(0.f),
+                      0xffffffffu);
 }
 
 // ---------------------------------------------------------------------------
