@@ -610,7 +610,7 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   TREVS_TRY(record(a->events, 5, s));
 
   TREVS_TRY(record(a->events, 6, s));
-  TREVS_HIP(launch_topk(score, a->B, a->K_in, a->k_keep, a->kept_idx, s));
+  TREVS_HIP(launch_topk(score, a->B, a->K_in, a->k_keep, a->kept_idx, s, /*nonneg=*/true));  // means of probabilities
   TREVS_TRY(record(a->events, 7, s));
 
   const int So = a->S - a->K_in + a->k_keep;

@@ -203,7 +203,10 @@ hipError_t launch_prellm_select(const SelArgs& a, int B, hipStream_t s);
 // Budget-split selection: the K_t highest s^t, then the K - K_t highest s^v
 // among the other tokens.
 hipError_t launch_budget_select(const SelArgs& a, int B, hipStream_t s);
-hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, hipStream_t s);
+// Stable top-K per row; nonneg: every score is >= 0 (lets the selection skip
+// its min/max reduction).
+hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, hipStream_t s,
+                       bool nonneg = false);
 hipError_t launch_stats(const StatsArgs& a, int dtype, int dh, hipStream_t s);
 hipError_t launch_heads(const HeadArgs& a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs& a, int dtype, int dh, hipStream_t s);

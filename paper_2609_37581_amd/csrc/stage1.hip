@@ -749,7 +749,7 @@ __global__ __launch_bounds__(kSelThreads) void budget_topk_kernel(SelArgs a) {
 
 template <int E>
 __global__ __launch_bounds__(kSelThreads) void topk_kernel(const float* scores, int N, int K,
-                                                           int32_t* out) {
+                                                           int32_t* out, bool nonneg) {
   __shared__ SelectShared sh;
   const int b = blockIdx.x, tid = threadIdx.x;
   const float* p = scores + (size_t)b * N;
@@ -759,7 +759,8 @@ __global__ __launch_bounds__(kSelThreads) void topk_kernel(const float* scores, 
 #pragma unroll
   for (int e = 0; e < E; ++e)
     if (e * kSelThreads + tid >= N) sc[e] = 0.f;
-  block_topk_write<E>(sc, N, K, out + (size_t)b * K, sh);
+  // scores known to be >= 0 bound the keys by [key(+0), 0xffffffff]: no min/max reduction
+  block_topk_write<E>(sc, N, K, out + (size_t)b * K, sh, nonneg, f2key(0.f), 0xffffffffu);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -931,8 +932,9 @@ hipError_t launch_budget_select(const SelArgs& a, int B, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, hipStream_t s) {
-#define CALL(E) hipLaunchKernelGGL(topk_kernel<E>, dim3(B), dim3(kSelThreads), 0, s, scores, N, K, out)
+hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, hipStream_t s,
+                       bool nonneg) {
+#define CALL(E) hipLaunchKernelGGL(topk_kernel<E>, dim3(B), dim3(kSelThreads), 0, s, scores, N, K, out, nonneg)
   TREVS_SELECT_SWITCH(select_e(N), CALL)
 #undef CALL
   return hipGetLastError();
