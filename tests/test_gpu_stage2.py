@@ -163,6 +163,31 @@ def test_stage2_max_visual_rows(k_keep):
         assert np.array_equal(g["hidden_out"], inp["hidden"])
 
 
+def test_stage2_identical_visual_keys_keep_the_first_tokens():
+    """All visual keys equal: every token gets the same score (uniform
+    attention over the visual block), so the stable top-K keeps the lowest
+    indices; the score selection then resolves a single all-equal key."""
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=2)
+    inp = stage2_inputs(w)
+    k = inp["k"].copy()
+    k[:, w.P:w.P + w.K1] = k[:, w.P:w.P + 1]
+    inp = dict(inp, k=k)
+    print("[stage2] identical visual keys", flush=True)
+    g = run_gpu(inp, w)
+    # every head's variance is 0 up to rounding (the one-pass form leaves
+    # ~1e-12 either side), so the head set is any; score with the kernel's
+    o = run_oracle(inp, w, w.n_keep, w.K2, heads=g["head_sel"])
+    assert np.abs(g["head_var"]).max() < 1e-9
+    assert_scores_close(g["score"], o["score"], "p")
+    S = inp["hidden"].shape[1]
+    for b in range(w.B):
+        assert (g["score"][b] == g["score"][b][0]).all(), b
+        assert np.array_equal(g["kept_idx"][b], np.arange(w.K2)), b
+        assert np.array_equal(o["kept_idx"][b], np.arange(w.K2)), b
+        rows = oracle.compaction_rows(S, w.P, w.K1, g["kept_idx"][b])
+        assert np.array_equal(g["hidden_out"][b], inp["hidden"][b][rows]), b
+
+
 def test_stage2_text_lengths_out_of_range_are_clamped():
     """Device-resident text lengths are clamped into 1..T_max by the kernels:
     0 and T_max + 7 behave as 1 and T_max (bit for bit)."""
