@@ -78,3 +78,36 @@ def assert_kept_exact_on_own_scores(gpu_idx, gpu_scores, k, name):
     for b in range(gpu_idx.shape[0]):
         want = oracle.topk_ascending(np.asarray(gpu_scores[b], dtype=np.float32).astype(np.float64), k)
         assert gpu_idx[b].tolist() == want.tolist(), f"{name}[{b}]: not the top-k of its own scores"
+
+
+FPS_TIE = 1e-5  # oracle distances this close are a genuine near-tie
+
+
+def check_fps_picks(Z64, pivots, picks, want):
+    """Every pick of the GPU sequence is valid against the GPU's own selected
+    set so far: it is not yet selected, and its float64 distance to its
+    nearest selected token is within FPS_TIE of the largest over the
+    unselected tokens.  Where the largest leads by more than FPS_TIE this
+    forces the unique farthest token, so the sequence equals the oracle's
+    `want` until a genuine near-tie, and every later pick is still checked
+    against the history the GPU actually took.  Returns the number of picks
+    equal to the oracle's before the first difference."""
+    zbar = oracle.l2_normalise_rows(Z64)
+    N = zbar.shape[0]
+    taken = np.zeros(N, dtype=bool)
+    taken[np.asarray(pivots, dtype=np.int64)] = True
+    dist = (1.0 - zbar @ zbar[np.asarray(pivots, dtype=np.int64)].T).min(axis=1) if len(pivots) \
+        else np.zeros(N)
+    same = 0
+    for t, p in enumerate(picks):
+        p = int(p)
+        assert 0 <= p < N and not taken[p], (t, p)
+        if not taken.any():  # nothing selected yet: the lowest index
+            assert p == 0, (t, p)
+        best = dist[~taken].max()
+        assert dist[p] >= best - FPS_TIE, (t, p, dist[p], best)
+        if same == t and p == int(want[t]):
+            same += 1
+        taken[p] = True
+        dist = np.minimum(dist, 1.0 - zbar @ zbar[p])
+    return same

@@ -7,7 +7,7 @@ import torch
 import oracle
 from paper_2609_37581_amd import trevs
 from parity import (assert_kept_band, assert_kept_exact_on_own_scores, assert_scores_close,
-                    dev_tensor, host_bits)
+                    check_fps_picks, dev_tensor, host_bits)
 from synthetic import WORKLOADS, stage1_inputs
 
 pytestmark = pytest.mark.gpu
@@ -276,13 +276,6 @@ def test_stage1_budget_split(name):
 
 
 # ------------------------------------------------------------- diversity set
-def _fps_distances(Z64, selected):
-    """Distance of every token to its nearest selected token, from the
-    oracle's normalised features (float64)."""
-    zbar = oracle.l2_normalise_rows(Z64)
-    return (1.0 - zbar @ zbar[np.asarray(selected)].T).min(axis=1)
-
-
 FPS_CASES = {
     "llava15-b2-bf16": (WORKLOADS["llava15-b64-bf16"].with_(B=2), 48),
     "llava15-b1-f32": (WORKLOADS["llava15-b1-f32"], 48),
@@ -304,10 +297,11 @@ FPS_CASES = {
 def test_stage1_diversity_set(name):
     """Context preservation by farthest point sampling (Sec. 4.1, after Eq.
     (7)).  The pivots are the exact top-K_r of the kernel's own fused score;
-    the picks follow the oracle's sequential rule from the same pivots, step
-    for step, unless a step is a genuine near-tie (the two candidates' oracle
-    distances within 1e-5), after which the sequences may legitimately part;
-    the kept list is the ascending union and the gather is bit-exact."""
+    every pick is the farthest unselected token from the GPU's own selected
+    set so far (within a 1e-5 near-tie of the float64 distances), which
+    forces the oracle's sequence until a genuine near-tie and checks every
+    pick after it; the kept list is the ascending union and the gather is
+    bit-exact."""
     w, k_div = FPS_CASES[name]
     print(f"[stage1-fps] {name}: B={w.B} N={w.N} K1={w.K1} K_d={k_div}", flush=True)
     inp = stage1_inputs(w)
@@ -334,13 +328,5 @@ def test_stage1_diversity_set(name):
         assert np.array_equal(feats[b], inp["vis_feats"][b][kept[b]]), b
         Z64 = oracle.to_f64(inp["vis_feats"][b], w.dtype)
         want = oracle.farthest_point_sampling(Z64, pivots, k_div)
-        sel = list(pivots)
-        for t in range(k_div):
-            if picks[b][t] == want[t]:
-                sel.append(int(picks[b][t]))
-                continue
-            d = _fps_distances(Z64, sel)
-            assert picks[b][t] not in sel, (b, t)
-            gap = abs(d[picks[b][t]] - d[want[t]])
-            assert gap <= 1e-5, (b, t, picks[b][t], want[t], gap)
-            break  # a near-tie: later picks may legitimately differ
+        same = check_fps_picks(Z64, pivots, picks[b], want)
+        print(f"[stage1-fps] {name} b={b}: {same}/{k_div} picks equal the oracle's sequence", flush=True)
