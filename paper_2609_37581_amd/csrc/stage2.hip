@@ -35,10 +35,13 @@ constexpr int stats_ring(int vectors_per_tile) { return vectors_per_tile >= 4 ? 
 // stream, so the extra work is spread evenly over the grid.  Every row sees
 // at least its own key, so the merged non-visual log-sum-exp is finite.
 // ---------------------------------------------------------------------------
-// (two-wave workgroups are held to four waves per SIMD: at 2048 of them,
-// LLaVA-1.5 batch 64, all are resident at once, 45.5 -> 43.3 us)
+// (two-wave workgroups over rows of at most 256 bytes are held to four waves
+// per SIMD: at 2048 of them, LLaVA-1.5 batch 64, all are resident at once,
+// 45.5 -> 43.3 us; wider rows hold too many Q registers for four)
+template <class In, int DH>
+constexpr int stats_min_waves(int NW) { return NW == 2 && DH * In::kBytes <= 256 ? 4 : 1; }
 template <class In, int DH, int NW, bool CAUSAL>
-__global__ __launch_bounds__(64 * NW, NW == 2 ? 4 : 1) void t2v_stats_kernel(StatsArgs a) {
+__global__ __launch_bounds__(64 * NW, (stats_min_waves<In, DH>(NW))) void t2v_stats_kernel(StatsArgs a) {
   constexpr int ROWB = DH * In::kBytes;
   constexpr int HALFB = ROWB / 2;
   constexpr int NF = HALFB / 64;

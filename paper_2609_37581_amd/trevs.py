@@ -76,6 +76,31 @@ class SensitivityArgs(ctypes.Structure):
                 ("head_var", c_void_p * 2), ("events", c_void_p), ("softmax", c_int32)]
 
 
+def _torch_empty(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+_alloc = _torch_empty
+
+
+def set_allocator(fn=None):
+    """Route every output and workspace allocation of this binding through
+    fn(shape, dtype, device) -> contiguous tensor (None: torch.empty).
+    Returns the previous allocator.  The tests use it to surround each
+    buffer with guard bands."""
+    global _alloc
+    prev = _alloc
+    _alloc = fn or _torch_empty
+    return prev
+
+
+def _empty(shape, dtype, device):
+    t = _alloc(tuple(shape), dtype, device)
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype or not t.is_contiguous():
+        raise RuntimeError("allocator returned a tensor of the wrong shape, dtype or layout")
+    return t
+
+
 _lib = None
 
 
@@ -191,19 +216,19 @@ class Prellm:
         if text_len is not None and text_len.shape != (B,):
             raise ValueError("text_len must be [B]")
         self.inputs = (cls_logits, vis_feats, text_emb, text_len)
-        self.kept_idx = torch.empty((B, k_keep), dtype=torch.int32, device=dev)
+        self.kept_idx = _empty((B, k_keep), torch.int32, dev)
         # farthest-point diversity tokens in pick order (k_div > 0)
-        self.div_idx = torch.empty((B, k_div), dtype=torch.int32, device=dev) if k_div > 0 else None
-        self.kept_feats = torch.empty((B, k_keep, d), dtype=dt, device=dev)
+        self.div_idx = _empty((B, k_div), torch.int32, dev) if k_div > 0 else None
+        self.kept_feats = _empty((B, k_keep, d), dt, dev)
         if ratio_mode not in RATIO_MODES:
             raise ValueError(f"ratio_mode must be one of {sorted(RATIO_MODES)}")
         budget = ratio_mode == "budget"
         if want_scores:
             # the budget split ranks the raw scores: no fused score, no Med/MAD
-            self.score = None if budget else torch.empty((B, N), dtype=torch.float32, device=dev)
-            self.sal = torch.empty((B, N), dtype=torch.float32, device=dev)
-            self.rel = torch.empty((B, N), dtype=torch.float32, device=dev)
-            self.norm_stats = None if budget else torch.empty((B, 4), dtype=torch.float32, device=dev)
+            self.score = None if budget else _empty((B, N), torch.float32, dev)
+            self.sal = _empty((B, N), torch.float32, dev)
+            self.rel = _empty((B, N), torch.float32, dev)
+            self.norm_stats = None if budget else _empty((B, 4), torch.float32, dev)
         else:
             self.score = self.sal = self.rel = self.norm_stats = None
         a = PrellmArgs()
@@ -225,7 +250,7 @@ class Prellm:
             # invalid arguments: let the call report the precise status
             st = lib().trevs_prellm_prune(ctypes.byref(a), None, 0, None)
             raise TrevsError(st, "trevs_prellm_prune")
-        self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.workspace = _empty((ws,), torch.uint8, dev)
 
     def __call__(self, stream=None, events=None):
         ev = _EventArray(events, PRELLM_NUM_KERNELS)
@@ -280,15 +305,15 @@ class Inllm:
             raise ValueError("lse_rest must be [B,H_q,T_max]")
         So = S - K_in + k_keep
         self.inputs = (q, k, v, hidden, pos, text_len, lse_rest)
-        self.kept_idx = torch.empty((B, k_keep), dtype=torch.int32, device=dev)
-        self.hidden_out = torch.empty((B, So, D), dtype=dt, device=dev)
-        self.k_out = torch.empty((B, So, H_kv, d_head), dtype=dt, device=dev)
-        self.v_out = torch.empty((B, So, H_kv, d_head), dtype=dt, device=dev)
-        self.pos_out = torch.empty((n_pos, B, So), dtype=torch.int64, device=dev)
+        self.kept_idx = _empty((B, k_keep), torch.int32, dev)
+        self.hidden_out = _empty((B, So, D), dt, dev)
+        self.k_out = _empty((B, So, H_kv, d_head), dt, dev)
+        self.v_out = _empty((B, So, H_kv, d_head), dt, dev)
+        self.pos_out = _empty((n_pos, B, So), torch.int64, dev)
         if want_scores:
-            self.head_sel = torch.empty((B, n_keep_heads), dtype=torch.int32, device=dev)
-            self.head_var = torch.empty((B, H_q), dtype=torch.float32, device=dev)
-            self.score = torch.empty((B, K_in), dtype=torch.float32, device=dev)
+            self.head_sel = _empty((B, n_keep_heads), torch.int32, dev)
+            self.head_var = _empty((B, H_q), torch.float32, dev)
+            self.score = _empty((B, K_in), torch.float32, dev)
         else:
             self.head_sel = self.head_var = self.score = None
         a = InllmArgs()
@@ -309,7 +334,7 @@ class Inllm:
         if ws == 0:
             st = lib().trevs_inllm_prune(ctypes.byref(a), None, 0, None)
             raise TrevsError(st, "trevs_inllm_prune")
-        self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.workspace = _empty((ws,), torch.uint8, dev)
 
     def __call__(self, stream=None, events=None):
         ev = _EventArray(events, INLLM_NUM_KERNELS)
@@ -337,7 +362,7 @@ def topk_select(scores, k, stream=None):
     ascending."""
     _check(scores, "scores", scores.device, 2, torch.float32)
     B, N = scores.shape
-    out = torch.empty((B, k), dtype=torch.int32, device=scores.device)
+    out = _empty((B, k), torch.int32, scores.device)
     st = lib().trevs_topk_select(scores.data_ptr(), B, N, k, out.data_ptr(), None, 0, _stream(stream))
     if st:
         raise TrevsError(st, "trevs_topk_select")
@@ -373,9 +398,9 @@ class TextSensitivity:
                 if t.shape != (B, H_q, T_max):
                     raise ValueError(f"{name} must be [B,H_q,T_max]")
         self.inputs = (q, k, q2, k2, text_len, text_len2, lse_rest, lse_rest2)
-        self.ts = torch.empty((B, H_q), dtype=torch.float32, device=dev)
-        self.profile = [torch.empty((B, H_q, K_in), dtype=torch.float32, device=dev) for _ in range(2)]
-        self.head_var = [torch.empty((B, H_q), dtype=torch.float32, device=dev) for _ in range(2)]
+        self.ts = _empty((B, H_q), torch.float32, dev)
+        self.profile = [_empty((B, H_q, K_in), torch.float32, dev) for _ in range(2)]
+        self.head_var = [_empty((B, H_q), torch.float32, dev) for _ in range(2)]
         a = SensitivityArgs()
         a.struct_size = ctypes.sizeof(SensitivityArgs)
         a.B, a.S, a.P, a.K_in, a.T_max = B, S, P, K_in, T_max
@@ -394,7 +419,7 @@ class TextSensitivity:
         if ws == 0:
             st = lib().trevs_text_sensitivity(ctypes.byref(a), None, 0, None)
             raise TrevsError(st, "trevs_text_sensitivity")
-        self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.workspace = _empty((ws,), torch.uint8, dev)
 
     def __call__(self, stream=None, events=None):
         ev = _EventArray(events, SENSITIVITY_NUM_KERNELS)
@@ -428,10 +453,10 @@ class TopkSpearman:
         self.inputs = (sv, st)
         self.B, self.N = sv.shape
         self.k = k
-        self.rho = torch.empty(self.B, dtype=torch.float64, device=sv.device)
-        self.kept_idx = torch.empty((self.B, k), dtype=torch.int32, device=sv.device)
+        self.rho = _empty((self.B,), torch.float64, sv.device)
+        self.kept_idx = _empty((self.B, k), torch.int32, sv.device)
         self.ws_bytes = lib().trevs_spearman_workspace_size(self.B, self.N, k)
-        self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=sv.device)
+        self.workspace = _empty((max(self.ws_bytes, 1),), torch.uint8, sv.device)
 
     def __call__(self, stream=None):
         sv, st = self.inputs

@@ -244,7 +244,9 @@ def stage2_inputs(w, with_lse_rest=False):
     Sequence layout [prefix P | K1 visual | T_max text].  Returns dict: q
     [B,S,H_q,d_h], k and v [B,S,H_kv,d_h], hidden [B,S,D], pos int64
     [n_pos,B,S], text_len int32 [B], optionally lse_rest float32 [B,H_q,T_max],
-    and the planted relevant visual rows and sensitive heads per sample."""
+    and the planted relevant visual rows and sensitive heads per sample.
+    With tie_stress a quarter of the visual key rows are copies of prototype
+    rows (exact ties in the token score)."""
     B, S, Hq, Hkv, dh, D = w.B, w.S, w.H_q, w.H_kv, w.d_h, w.D
     G = Hq // Hkv
     lens = _text_lengths(w)
@@ -273,6 +275,16 @@ def stage2_inputs(w, with_lse_rest=False):
             Kt[w.P + rel, g, :] += (a * c[g]).astype(np.float32)
         for h in sens:
             Q[w.P + w.K1:, h, :] += (a * c[h // G]).astype(np.float32)
+        if w.tie_stress and w.K1 >= 4:
+            # a quarter of the visual key rows copy one of (up to) 64
+            # prototype visual rows in every KV head: their logits, and so
+            # their token scores, tie exactly
+            n_proto = min(64, w.K1 // 4)
+            protos = rng.choice(w.K1, size=n_proto, replace=False)
+            others = np.setdiff1d(np.arange(w.K1), protos)
+            copies = rng.choice(others, size=w.K1 // 4, replace=False)
+            src = protos[rng.integers(0, n_proto, size=copies.size)]
+            Kt[w.P + copies] = Kt[w.P + src]
         kept_vis = np.sort(rng.choice(w.N, size=w.K1, replace=False))
         q[b] = to_storage(Q, w.dtype)
         k[b] = to_storage(Kt, w.dtype)

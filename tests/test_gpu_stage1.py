@@ -143,6 +143,31 @@ def test_stage1_single_token_and_constant_inputs():
     assert np.all(g2["score"] == 0)
 
 
+def test_stage1_text_median_and_mad_zero():
+    """More than half of the tokens have s^t = 0 exactly (their features are
+    orthogonal to every text row: disjoint supports), the rest are positive
+    outliers, so Med(s^t) = MAD(s^t) = 0 and Eq. (6)'s epsilon alone sets the
+    text branch's scale (s^t / eps, about 1e7)."""
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=2, N=500, d=256, M_max=40, K1=120, n_sal=4,
+                                            n_qm=0, text_len=("uniform", 10, 40))
+    inp = stage1_inputs(w)
+    rng = np.random.default_rng(11)
+    T = inp["text_emb"].copy()
+    Z = inp["vis_feats"].copy()
+    T[:, :, 32:] = 0  # text rows live on the first 32 coordinates
+    for b in range(w.B):
+        zero = rng.choice(w.N, size=3 * w.N // 5, replace=False)
+        Z[b][zero[:, None], np.arange(32)[None, :]] = 0  # orthogonal to every text row
+    inp = dict(inp, text_emb=T, vis_feats=Z)
+    g = run_gpu(inp, w)
+    o = run_oracle(inp, w)
+    for b in range(w.B):
+        assert o["med_t"][b] == 0.0 and o["mad_t"][b] == 0.0, b
+        assert (g["rel"][b] == 0).sum() >= 3 * w.N // 5, b
+    assert (g["norm_stats"][:, 2:] == 0).all()
+    check(inp, w, g, o)
+
+
 def test_stage1_identical_tokens_score_identically():
     """Position independence: tokens with identical inputs get bit-identical
     scores wherever they sit in the tiles."""
@@ -171,33 +196,18 @@ def qwen_full():
     return w, stage1_inputs(w)
 
 
-def test_stage1_full_size_qwen_sampled(qwen_full):
-    """The benchmarked launch configuration (B=4, N=16384, d'=3584, M=128):
-    s^v in full, s^t on sampled tokens computed one by one, and every later
-    step re-derived by the oracle from the kernel's own s^v and s^t."""
+def test_stage1_full_size_qwen(qwen_full):
+    """The benchmarked launch configuration (B=4, N=16384, d'=3584, M=128),
+    every score of every token against the full float64 oracle: s^v, s^t,
+    Med/MAD, the fused score, the kept band and the gather."""
     w, inp = qwen_full
     print("[stage1] full-size qwen", flush=True)
     g = run_gpu(inp, w)
-    rng = np.random.default_rng(0)
-    for b in range(w.B):
-        sv = oracle.cls_saliency(oracle.to_f64(inp["cls_logits"][b], "bf16"), w.n_seg)
-        assert_scores_close(g["sal"][b], sv, f"s^v[{b}]")
-        idx = np.unique(np.concatenate([rng.choice(w.N, 384, replace=False), inp["matched"][b][:64],
-                                        [0, w.N - 1]]))
-        T = oracle.to_f64(inp["text_emb"][b, :inp["text_len"][b]], "bf16")
-        st = oracle.text_relevance(oracle.to_f64(inp["vis_feats"][b][idx], "bf16"), T)
-        assert_scores_close(g["rel"][b][idx], st, f"s^t[{b}] sampled")
-        gsv = g["sal"][b].astype(np.float64)
-        gst = g["rel"][b].astype(np.float64)
-        hv, med_v, mad_v = oracle.robust_normalise(gsv, 1.4, 1e-8)
-        ht, med_t, mad_t = oracle.robust_normalise(gst, 1.0, 1e-8)
-        assert_scores_close(g["norm_stats"][b], [med_v, mad_v, med_t, mad_t], f"Med/MAD[{b}]")
-        s = oracle.fuse_scores(hv, ht, w.rho, 1.0)
-        assert_scores_close(g["score"][b], s, f"s[{b}]")
-        assert_kept_band(g["kept_idx"][b:b + 1], s[None], w.K1, f"kept[{b}]")
-        assert np.array_equal(g["kept_feats"][b], inp["vis_feats"][b][g["kept_idx"][b]])
-    assert_kept_exact_on_own_scores(g["kept_idx"], g["score"], w.K1, "kept")
-    # planted structure survives: most query-matched tokens are kept
+    print("[stage1] full-size qwen: oracle", flush=True)
+    o = run_oracle(inp, w)
+    check(inp, w, g, o)
+    # planted structure survives: the oracle keeps every query-matched token
+    # on these inputs, the kernel nearly all
     for b in range(w.B):
         assert np.isin(inp["matched"][b], g["kept_idx"][b]).mean() > 0.9
 

@@ -211,10 +211,15 @@ def test_stage2_full_size_qwen(qwen_full):
     w, inp = qwen_full
     print("[stage2] full-size qwen", flush=True)
     g = run_gpu(inp, w)
-    check(inp, w, g)
-    # planted structure: the sensitive heads have the highest variance
+    o = check(inp, w, g)
+    # planted structure: the relevant tokens are mostly kept.  The method
+    # itself (the oracle) keeps 0.87-0.94 of them on these inputs, so the
+    # floor is 0.8, and the kernel's recall matches the oracle's up to the
+    # tie band
     for b in range(w.B):
-        assert np.isin(inp["relevant"][b], g["kept_idx"][b]).mean() > 0.8
+        rg = np.isin(inp["relevant"][b], g["kept_idx"][b]).mean()
+        ro = np.isin(inp["relevant"][b], o["kept_idx"][b]).mean()
+        assert ro > 0.8 and abs(rg - ro) <= 0.01, (b, rg, ro)
 
 
 def test_stage2_full_size_qwen_causal(qwen_full):

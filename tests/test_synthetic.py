@@ -56,3 +56,14 @@ def test_sweep_grid():
     g = sweep()
     assert len(g) == 4 * 5 * 4
     assert sorted({(c.K1, c.K2) for c in g}) == [(32, 11), (64, 21), (144, 48), (288, 96)]
+
+
+def test_stage2_tie_stress_copies_visual_key_rows():
+    w = WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, K1=144, D=8, tie_stress=True)
+    s = stage2_inputs(w)
+    for b in range(w.B):
+        vis = s["k"][b, w.P:w.P + w.K1].reshape(w.K1, -1)
+        n_distinct = np.unique(vis, axis=0).shape[0]
+        assert n_distinct == w.K1 - w.K1 // 4  # every copy repeats a prototype row
+    plain = stage2_inputs(w.with_(tie_stress=False))
+    assert np.unique(plain["k"][0, w.P:w.P + w.K1].reshape(w.K1, -1), axis=0).shape[0] == w.K1
