@@ -68,15 +68,31 @@ def counter_traffic(workload):
     return float(vals["hbm_bytes_per_launch"])
 
 
+def cpu_info():
+    """Host CPU model, the cores this process may run on, and the BLAS
+    library's thread count (the threads the oracle's matrix products use)."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    affinity = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        blas = affinity
+    return model, affinity, blas
+
+
 def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights", k_div=0, softmax="visual"):
     """The CPU oracle as it stands, on single samples of the same workload,
     repeated until about budget_s seconds of work."""
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # noqa: BLE001
-        threads = len(os.sched_getaffinity(0))
+    model, affinity, threads = cpu_info()
     t0 = time.perf_counter()
     n = 0
     while True:
@@ -93,7 +109,9 @@ def cpu_baseline(w, s1, s2, budget_s, ratio_mode="weights", k_div=0, softmax="vi
             break
     return {"value": n * w.N / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{n} single samples (B=1) of {w.name}, both stages, float64 NumPy, "
-                      f"{el:.1f} s"}
+                      f"{el:.1f} s",
+            "cpu_model": model, "affinity_cores": affinity, "blas_threads": int(threads),
+            "latency_ms_per_sample": el / n * 1e3}
 
 
 def profile_flops(w, text_len):
@@ -117,9 +135,10 @@ def cpu_baseline_analysis(w, si, sv, st, budget_s):
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
-    return {"value": n / el, "unit": "samples/s", "cores": len(os.sched_getaffinity(0)),
-            "kind": "oracle",
-            "sample": f"{n} single samples (B=1) of the analysis on {w.name}, float64 NumPy, {el:.1f} s"}
+    model, affinity, threads = cpu_info()
+    return {"value": n / el, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} single samples (B=1) of the analysis on {w.name}, float64 NumPy, {el:.1f} s",
+            "cpu_model": model, "affinity_cores": affinity, "blas_threads": int(threads)}
 
 
 def run_analysis(args, w):
@@ -229,6 +248,68 @@ def run_analysis(args, w):
     print(json.dumps(result), flush=True)
 
 
+def stage_latency(pre, inl, stream, n, trevs):
+    """Per-step and per-stage latencies (ms) from a separate pass of n steps
+    with a HIP event before stage 1, between the stages and after stage 2 on
+    the launch stream."""
+    ev = trevs.HipEvents(3 * n)
+    for i in range(n):
+        ev.record(3 * i, stream)
+        pre(stream)
+        ev.record(3 * i + 1, stream)
+        inl(stream)
+        ev.record(3 * i + 2, stream)
+    stream.synchronize()
+    t1 = np.array([ev.elapsed_ms(3 * i, 3 * i + 1) for i in range(n)])
+    t2 = np.array([ev.elapsed_ms(3 * i + 1, 3 * i + 2) for i in range(n)])
+    ev.close()
+    return t1, t2
+
+
+def graph_step_ms(pre, inl, steps, warmup):
+    """Both stages captured once into a HIP graph (torch.cuda.CUDAGraph over
+    the library's launches; the path records no memset) and replayed: the
+    same kernels with the per-launch host work removed."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        pre(side)
+        inl(side)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pre()
+        inl()
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
+def plain_step_ms(pre, inl, stream, steps, warmup):
+    """ms per step of both stages, no events inside the timed region."""
+    import torch
+    for _ in range(warmup):
+        pre(stream)
+        inl(stream)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        pre(stream)
+        inl(stream)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -327,6 +408,20 @@ def main():
             kern_ms[n] += ev.elapsed_ms(base + 2 * j, base + 2 * j + 1) / nb_steps
     ev.close()
 
+    # step and stage latency distribution (separate pass, events at the stage
+    # boundaries)
+    t1, t2 = stage_latency(pre, inl, stream, args.steps, trevs)
+    tstep = t1 + t2
+    # the same step replayed from a captured HIP graph
+    g_ms = graph_step_ms(pre, inl, args.steps, args.warmup)
+    # the stage-2 softmax over each text row's whole causal row (Sec. 4.2's
+    # text-to-vision attention within the layer's own attention)
+    other = "causal" if args.softmax == "visual" else "visual"
+    inl_other = trevs.Inllm(q, k, v, hid, pos, tl2, P=w.P, K_in=w.K1, n_keep_heads=w.n_keep,
+                            k_keep=w.K2, softmax=other)
+    other_ms = plain_step_ms(pre, inl_other, stream, args.steps, args.warmup)
+    del inl_other
+
     # device copy bandwidth of the same run (context, and the reference kernel
     # for scaling the HBM counters of a profile)
     nbytes = 1 << 30
@@ -370,7 +465,19 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": traffic, "bytes_per_launch": nb["relevance"]},
         "path_hbm_frac": nb["total"] / t_step / 1e9 / HBM_PEAK_GBPS,
+        "path_hbm_target": 0.60,
         "path_bytes": nb,
+        "latency_ms": {"p50": float(np.percentile(tstep, 50)), "p90": float(np.percentile(tstep, 90)),
+                       "stage1_p50": float(np.percentile(t1, 50)), "stage1_p90": float(np.percentile(t1, 90)),
+                       "stage2_p50": float(np.percentile(t2, 50)), "stage2_p90": float(np.percentile(t2, 90)),
+                       "pass": f"{args.steps} steps, HIP events at the stage boundaries"},
+        "stage_rates": {"stage1_tokens_per_s": w.B * w.N / (np.percentile(t1, 50) * 1e-3),
+                        "stage2_tokens_per_s": w.B * w.K1 / (np.percentile(t2, 50) * 1e-3),
+                        "stage1_hbm_frac": nb["stage1"] / (np.percentile(t1, 50) * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                        "stage2_hbm_frac": nb["stage2"] / (np.percentile(t2, 50) * 1e-3) / 1e9 / HBM_PEAK_GBPS},
+        "graph_replay": {"ms_per_step": g_ms, "value": tokens / (g_ms * 1e-3),
+                         "path_hbm_frac": nb["total"] / (g_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS},
+        f"softmax_{other}": {"ms_per_step": other_ms, "value": tokens / (other_ms * 1e-3)},
         "relevance_us": rel_ms * 1e3,
         "kernels_us_separate_pass": {n: round(v * 1e3, 3) for n, v in kern_ms.items()},
         "copy_gbps": copy_gbps,
