@@ -264,6 +264,27 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* args, void* workspace,
 trevs_status trevs_inllm_prune(const trevs_inllm_args* args, void* workspace,
                                size_t workspace_bytes, void* stream);
 
+/* Stage 2 exactly as trevs_inllm_prune, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid allocation.  The caller passes inputs and outputs
+ * only; the workspace is a static device array of
+ * TREVS_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held from the
+ * first call on that GPU until the process ends.  The call allocates and
+ * frees nothing.
+ *   - Runs on the calling thread's current device, which must be the
+ *     stream's device.  The first call on a device looks up the array's
+ *     address there (hipGetSymbolAddress); make that first call before
+ *     capturing a graph.
+ *   - Arguments whose workspace (trevs_inllm_workspace_size) exceeds
+ *     TREVS_NOALLOC_SCRATCH_BYTES return TREVS_ERR_WORKSPACE before any
+ *     launch; invalid arguments return the status trevs_inllm_prune gives.
+ *   - Every call on a GPU shares that GPU's array: calls that overlap on one
+ *     GPU (different streams, or host threads) race and give undefined
+ *     results.  Serialise them, e.g. on one stream.  Calls in order on one
+ *     stream are safe; no state carries from one call to the next. */
+#define TREVS_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+trevs_status trevs_inllm_prune_noalloc(const trevs_inllm_args* args, void* stream);
+
 /* Stable top-K of each row of scores [B,N] (device, finite fp32): writes the
  * K kept indices of row b, ascending, to kept_idx [B,K].  N in
  * 1..TREVS_MAX_SELECT_N, K in 1..N.  Needs no workspace (pass NULL, 0). */

@@ -122,6 +122,8 @@ def lib():
         L.trevs_prellm_prune.restype = ctypes.c_int
         L.trevs_inllm_prune.argtypes = [ctypes.POINTER(InllmArgs), c_void_p, c_size_t, c_void_p]
         L.trevs_inllm_prune.restype = ctypes.c_int
+        L.trevs_inllm_prune_noalloc.argtypes = [ctypes.POINTER(InllmArgs), c_void_p]
+        L.trevs_inllm_prune_noalloc.restype = ctypes.c_int
         L.trevs_topk_select.argtypes = [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                         c_size_t, c_void_p]
         L.trevs_topk_select.restype = ctypes.c_int
@@ -278,7 +280,7 @@ class Inllm:
     """Stage 2 with outputs and workspace allocated once; call() enqueues it."""
 
     def __init__(self, q, k, v, hidden, pos, text_len=None, *, P, K_in, n_keep_heads, k_keep,
-                 scale=None, lse_rest=None, want_scores=False, softmax="visual"):
+                 scale=None, lse_rest=None, want_scores=False, softmax="visual", noalloc=False):
         dev = hidden.device
         _check(hidden, "hidden", dev, 3)
         dt = hidden.dtype
@@ -334,16 +336,21 @@ class Inllm:
         if ws == 0:
             st = lib().trevs_inllm_prune(ctypes.byref(a), None, 0, None)
             raise TrevsError(st, "trevs_inllm_prune")
-        self.workspace = _empty((ws,), torch.uint8, dev)
+        # noalloc: the library's static per-GPU workspace (trevs_inllm_prune_noalloc)
+        self.noalloc = noalloc
+        self.workspace = None if noalloc else _empty((ws,), torch.uint8, dev)
 
     def __call__(self, stream=None, events=None):
         ev = _EventArray(events, INLLM_NUM_KERNELS)
         self.args.events = ev.ptr
-        st = lib().trevs_inllm_prune(ctypes.byref(self.args), self.workspace.data_ptr(),
-                                     self.workspace.numel(), _stream(stream))
+        if self.noalloc:
+            st = lib().trevs_inllm_prune_noalloc(ctypes.byref(self.args), _stream(stream))
+        else:
+            st = lib().trevs_inllm_prune(ctypes.byref(self.args), self.workspace.data_ptr(),
+                                         self.workspace.numel(), _stream(stream))
         self.args.events = None
         if st:
-            raise TrevsError(st, "trevs_inllm_prune")
+            raise TrevsError(st, "trevs_inllm_prune_noalloc" if self.noalloc else "trevs_inllm_prune")
         return self.kept_idx, self.hidden_out, self.k_out, self.v_out, self.pos_out
 
 

@@ -223,3 +223,17 @@ def test_spearman_rejects_before_launch():
     assert L.trevs_topk_spearman(sv, st, 2, 40000, 30, rho, idx, ws, need, None) == 2
     assert L.trevs_topk_spearman(sv, st, 2, 100, 30, rho, idx, ws, need - 1, None) == 3
     assert L.trevs_topk_spearman(sv, st, 2, 100, 30, rho, idx, None, 0, None) == 3
+
+
+def test_noalloc_rejects_on_the_host():
+    """The allocation-free stage-2 entry point returns the regular entry
+    point's status for invalid arguments, and TREVS_ERR_WORKSPACE when the
+    call would need more than its static workspace, both before any HIP call."""
+    L = trevs.lib()
+    a = _inllm(k_keep=0)
+    assert L.trevs_inllm_prune_noalloc(ctypes.byref(a), None) == 1
+    # 64 samples x 32 heads x 1024 text rows of split statistics: > 16 MiB
+    big = _inllm(B=64, T_max=1024, S=35 + 192 + 1024)
+    need = L.trevs_inllm_workspace_size(ctypes.byref(big))
+    assert need > 16 << 20
+    assert L.trevs_inllm_prune_noalloc(ctypes.byref(big), None) == 3
