@@ -483,21 +483,30 @@ def topk_spearman(sv, st, k, stream=None):
 
 
 # ---------------------------------------------------------------- HIP events
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000  # hipEventDisableSystemFence
+
+
 class HipEvents:
     """A pool of hipEvent_t handles created through the HIP runtime that torch
-    has already loaded, for the per-kernel event slots of the entry points."""
+    has already loaded, for the per-kernel event slots of the entry points.
+
+    The events serve timing only, so they are created without the
+    system-scope release fence (hipEventDisableSystemFence): a fenced record
+    between two kernels writes back and invalidates the caches, which adds
+    several microseconds to the work it brackets.  Read the times only after
+    a device or stream synchronisation."""
 
     def __init__(self, n):
         self.rt = ctypes.CDLL("libamdhip64.so")
-        self.rt.hipEventCreate.argtypes = [ctypes.POINTER(c_void_p)]
+        self.rt.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(c_void_p), ctypes.c_uint]
         self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), c_void_p, c_void_p]
         self.rt.hipEventDestroy.argtypes = [c_void_p]
         self.rt.hipEventRecord.argtypes = [c_void_p, c_void_p]
         self.handles = []
         for _ in range(n):
             h = c_void_p()
-            if self.rt.hipEventCreate(ctypes.byref(h)):
-                raise RuntimeError("hipEventCreate failed")
+            if self.rt.hipEventCreateWithFlags(ctypes.byref(h), HIP_EVENT_DISABLE_SYSTEM_FENCE):
+                raise RuntimeError("hipEventCreateWithFlags failed")
             self.handles.append(h.value)
 
     def record(self, i, stream=None):
