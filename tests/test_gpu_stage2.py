@@ -86,6 +86,39 @@ CASES = {
 }
 
 
+GQA_CASES = {
+    # 2 text blocks, text lengths 16..64 (a sample's second block may be empty)
+    "gqa-b64-8/2-ragged-text": (WORKLOADS["llava15-b64-bf16"].with_(H_q=8, H_kv=2, D=64, n_keep=4), None),
+    # d_head 64, 4 text blocks of which many are past the text, 600 visual
+    # rows (the last token block partly empty)
+    "gqa-12/3-dh64-ragged": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=40, K1=600, K2=150, M_max=100, text_len=("uniform", 1, 100), H_q=12, H_kv=3, d_h=64,
+        D=64, n_keep=5, N=1200, grid=40), None),
+    # MQA with 12 query heads: the single run of 10 selected heads takes two steps
+    "mqa-12/1-run-split": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=32, K1=512, K2=100, M_max=64, H_q=12, H_kv=1, D=64, n_keep=10, N=1024, grid=32), None),
+    "gqa-f32-dh64": (WORKLOADS["llava15-b1-f32"].with_(
+        B=32, K1=300, K2=60, M_max=40, H_q=8, H_kv=4, d_h=64, D=32, n_keep=3, N=600), None),
+    # the 16,384-token model's heads (28/4, M-RoPE) at batch 2: every head, one head
+    "qwen-b2-all-heads": (WORKLOADS["qwen25vl-b4-bf16"].with_(B=2), 28),
+    "qwen-b2-one-head": (WORKLOADS["qwen25vl-b4-bf16"].with_(B=2), 1),
+}
+
+
+@pytest.mark.parametrize("name", list(GQA_CASES))
+def test_stage2_gqa_shapes(name):
+    """Grouped-query and multi-query attention at unsplit token-score grids:
+    key groups shared by 2 to 12 query heads, runs of selected heads in one
+    group, ragged text and visual blocks, all heads and one head."""
+    w, nk = GQA_CASES[name]
+    nk = nk or w.n_keep
+    print(f"[stage2-gqa] {name}: B={w.B} K1={w.K1} T={w.T_max} H={w.H_q}/{w.H_kv} dh={w.d_h} "
+          f"n_keep={nk} {w.dtype}", flush=True)
+    inp = stage2_inputs(w)
+    g = run_gpu(inp, w, n_keep=nk)
+    check(inp, w, g, n_keep=nk)
+
+
 @pytest.mark.parametrize("name", list(CASES))
 def test_stage2_parity(name):
     w = CASES[name]
