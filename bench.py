@@ -325,6 +325,8 @@ def main():
     ap.add_argument("--softmax", default="visual", choices=["visual", "causal"],
                     help="stage-2 softmax over the visual keys (default) or each text row's "
                          "whole causal row")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the latency, graph-replay and other-softmax passes (profiling runs)")
     ap.add_argument("--analysis", action="store_true",
                     help="time the Sec. 3 diagnostics (text sensitivity + Spearman) instead")
     args = ap.parse_args()
@@ -410,17 +412,33 @@ def main():
 
     # step and stage latency distribution (separate pass, events at the stage
     # boundaries)
-    t1, t2 = stage_latency(pre, inl, stream, args.steps, trevs)
-    tstep = t1 + t2
-    # the same step replayed from a captured HIP graph
-    g_ms = graph_step_ms(pre, inl, args.steps, args.warmup)
-    # the stage-2 softmax over each text row's whole causal row (Sec. 4.2's
-    # text-to-vision attention within the layer's own attention)
-    other = "causal" if args.softmax == "visual" else "visual"
-    inl_other = trevs.Inllm(q, k, v, hid, pos, tl2, P=w.P, K_in=w.K1, n_keep_heads=w.n_keep,
-                            k_keep=w.K2, softmax=other)
-    other_ms = plain_step_ms(pre, inl_other, stream, args.steps, args.warmup)
-    del inl_other
+    extras = {}
+    if not args.no_extras:
+        t1, t2 = stage_latency(pre, inl, stream, args.steps, trevs)
+        tstep = t1 + t2
+        extras["latency_ms"] = {
+            "p50": float(np.percentile(tstep, 50)), "p90": float(np.percentile(tstep, 90)),
+            "stage1_p50": float(np.percentile(t1, 50)), "stage1_p90": float(np.percentile(t1, 90)),
+            "stage2_p50": float(np.percentile(t2, 50)), "stage2_p90": float(np.percentile(t2, 90)),
+            "pass": f"{args.steps} steps, HIP events at the stage boundaries"}
+        nb_ = algorithmic_bytes(w, s1["text_len"], args.softmax)
+        t1s, t2s = np.percentile(t1, 50) * 1e-3, np.percentile(t2, 50) * 1e-3
+        extras["stage_rates"] = {"stage1_tokens_per_s": w.B * w.N / t1s,
+                                 "stage2_tokens_per_s": w.B * w.K1 / t2s,
+                                 "stage1_hbm_frac": nb_["stage1"] / t1s / 1e9 / HBM_PEAK_GBPS,
+                                 "stage2_hbm_frac": nb_["stage2"] / t2s / 1e9 / HBM_PEAK_GBPS}
+        # the same step replayed from a captured HIP graph
+        g_ms = graph_step_ms(pre, inl, args.steps, args.warmup)
+        extras["graph_replay"] = {"ms_per_step": g_ms, "value": w.B * w.N / (g_ms * 1e-3),
+                                  "path_hbm_frac": nb_["total"] / (g_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+        # the stage-2 softmax over each text row's whole causal row (Sec. 4.2's
+        # text-to-vision attention within the layer's own attention)
+        other = "causal" if args.softmax == "visual" else "visual"
+        inl_other = trevs.Inllm(q, k, v, hid, pos, tl2, P=w.P, K_in=w.K1, n_keep_heads=w.n_keep,
+                                k_keep=w.K2, softmax=other)
+        other_ms = plain_step_ms(pre, inl_other, stream, args.steps, args.warmup)
+        extras[f"softmax_{other}"] = {"ms_per_step": other_ms, "value": w.B * w.N / (other_ms * 1e-3)}
+        del inl_other
 
     # device copy bandwidth of the same run (context, and the reference kernel
     # for scaling the HBM counters of a profile)
@@ -467,17 +485,7 @@ def main():
         "path_hbm_frac": nb["total"] / t_step / 1e9 / HBM_PEAK_GBPS,
         "path_hbm_target": 0.60,
         "path_bytes": nb,
-        "latency_ms": {"p50": float(np.percentile(tstep, 50)), "p90": float(np.percentile(tstep, 90)),
-                       "stage1_p50": float(np.percentile(t1, 50)), "stage1_p90": float(np.percentile(t1, 90)),
-                       "stage2_p50": float(np.percentile(t2, 50)), "stage2_p90": float(np.percentile(t2, 90)),
-                       "pass": f"{args.steps} steps, HIP events at the stage boundaries"},
-        "stage_rates": {"stage1_tokens_per_s": w.B * w.N / (np.percentile(t1, 50) * 1e-3),
-                        "stage2_tokens_per_s": w.B * w.K1 / (np.percentile(t2, 50) * 1e-3),
-                        "stage1_hbm_frac": nb["stage1"] / (np.percentile(t1, 50) * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-                        "stage2_hbm_frac": nb["stage2"] / (np.percentile(t2, 50) * 1e-3) / 1e9 / HBM_PEAK_GBPS},
-        "graph_replay": {"ms_per_step": g_ms, "value": tokens / (g_ms * 1e-3),
-                         "path_hbm_frac": nb["total"] / (g_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS},
-        f"softmax_{other}": {"ms_per_step": other_ms, "value": tokens / (other_ms * 1e-3)},
+        **extras,
         "relevance_us": rel_ms * 1e3,
         "kernels_us_separate_pass": {n: round(v * 1e3, 3) for n, v in kern_ms.items()},
         "copy_gbps": copy_gbps,
