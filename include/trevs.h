@@ -146,6 +146,9 @@ typedef struct trevs_prellm_args {
  *                uses the row's KV head h/G.  A thus holds the visual columns
  *                of the layer's own attention matrix (Sec. 4.2).
  *   u_h      = (1/T_b) sum_q Var_i A[h,q,i]  (population variance)    Eq. (8)
+ *              (with row_stats: (1/T_b) sum_q [S2/K_in - (S1/K_in)^2] from the
+ *              caller's per-row sums S1 = sum_i A, S2 = sum_i A^2, and the
+ *              row log-sum-exp from row_stats as well)
  *   H*       = the n_keep_heads heads first under (u desc, h asc)
  *   p_i      = max_{q<T_b} (1/|H*|) sum_{h in H*} A[h,q,i]            Eq. (9)
  *   kept_idx = TopK(p, k_keep) ascending, relative to the visual block
@@ -191,6 +194,14 @@ typedef struct trevs_inllm_args {
   float* score_out;          /* OPTIONAL OUT [B,K_in] p_i */
   void* const* events;       /* OPTIONAL [2*TREVS_INLLM_NUM_KERNELS] hipEvent_t */
   int32_t softmax;           /* trevs_softmax: domain of the attention softmax (0 = VISUAL) */
+  const float* row_stats;    /* OPTIONAL [B,H_q,T_max,3] per text row, from the layer's own
+                                attention pass: (log-sum-exp of the row's logits over its
+                                softmax domain, natural log; sum and sum of squares of A over
+                                the K_in visual columns).  When given, u_h is formed from them
+                                and the row log-sum-exp is taken from them instead of being
+                                recomputed from q and k (softmax is then ignored and lse_rest
+                                must be NULL); the token score still recomputes the logits of
+                                the H* heads.  Rows q >= T_b are not read for u_h. */
 } trevs_inllm_args;
 
 /* ------------------------------------------------------------------------

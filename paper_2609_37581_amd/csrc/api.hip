@@ -160,6 +160,8 @@ trevs_status validate_inllm(const trevs_inllm_args* a) {
   if (!finite(a->scale) || a->scale <= 0.f) return TREVS_ERR_INVALID_ARG;
   if (a->softmax != TREVS_SOFTMAX_VISUAL && a->softmax != TREVS_SOFTMAX_CAUSAL) return TREVS_ERR_INVALID_ARG;
   if (a->softmax == TREVS_SOFTMAX_CAUSAL && a->lse_rest) return TREVS_ERR_INVALID_ARG;
+  if (a->row_stats && a->lse_rest) return TREVS_ERR_INVALID_ARG;  // the given statistics hold the domain
+  if (!aligned(a->row_stats, 4)) return TREVS_ERR_INVALID_ARG;
   if (!a->q || !a->k || !a->v || !a->hidden || !a->pos || !a->kept_idx || !a->hidden_out ||
       !a->k_out || !a->v_out || !a->pos_out)
     return TREVS_ERR_INVALID_ARG;
@@ -180,7 +182,8 @@ trevs_status validate_inllm(const trevs_inllm_args* a) {
                      {a->hidden, B * S * a->D * e},
                      {a->pos, (size_t)a->n_pos * B * S * 8},
                      {a->text_len, a->text_len ? B * 4 : 0},
-                     {a->lse_rest, a->lse_rest ? B * a->H_q * a->T_max * 4 : 0}};
+                     {a->lse_rest, a->lse_rest ? B * a->H_q * a->T_max * 4 : 0},
+                     {a->row_stats, a->row_stats ? B * a->H_q * a->T_max * 12 : 0}};
   const Span out[] = {{a->kept_idx, B * a->k_keep * 4},
                       {a->hidden_out, B * So * a->D * e},
                       {a->k_out, B * So * kvrow},
@@ -189,7 +192,7 @@ trevs_status validate_inllm(const trevs_inllm_args* a) {
                       {a->head_sel, a->head_sel ? B * a->n_keep_heads * 4 : 0},
                       {a->head_var, a->head_var ? B * a->H_q * 4 : 0},
                       {a->score_out, a->score_out ? B * a->K_in * 4 : 0}};
-  if (any_overlap(out, 8, in, 7)) return TREVS_ERR_INVALID_ARG;
+  if (any_overlap(out, 8, in, 8)) return TREVS_ERR_INVALID_ARG;
   if (a->d_head != 64 && a->d_head != 128 && a->d_head != 256) return TREVS_ERR_UNSUPPORTED;
   if (a->H_q > 256) return TREVS_ERR_UNSUPPORTED;
   if (a->K_in > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
@@ -223,15 +226,16 @@ size_t lse_rows_padded(int T_max) { return (size_t)(T_max + 31) / 32 * 32; }
 
 InllmPlan inllm_plan(const trevs_inllm_args* a) {
   InllmPlan p;
-  const StatsPlan sp = stats_plan(a->B, a->K_in, a->T_max, a->H_q, a->H_kv, a->softmax, a->P);
+  const StatsPlan sp = stats_plan(a->B, a->K_in, a->T_max, a->H_q, a->H_kv,
+                                  a->row_stats ? TREVS_SOFTMAX_VISUAL : a->softmax, a->P);
   p.n_split = sp.n_split;
   p.split_len = sp.split_len;
   p.n_rgroups = sp.n_rgroups;
   p.rest_len = sp.rest_len;
   const size_t rows = (size_t)a->B * a->H_q * a->T_max;
   size_t off = 0;
-  p.part = off;
-  off = align_up(off + rows * p.n_split * sizeof(float4));
+  p.part = off;  // split statistics (none with the caller's row statistics)
+  off = align_up(off + (a->row_stats ? 0 : rows * p.n_split * sizeof(float4)));
   p.part_rest = off;
   off = align_up(off + (p.rest_len ? rows * p.n_split * sizeof(float4) : 0));
   p.lse2 = off;
@@ -562,7 +566,7 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   ta.rest_len = p.rest_len;
   ta.part_rest = part_rest;
   TREVS_TRY(record(a->events, 0, s));
-  TREVS_HIP(launch_stats(ta, a->dtype, a->d_head, s));
+  if (!a->row_stats) TREVS_HIP(launch_stats(ta, a->dtype, a->d_head, s));
   TREVS_TRY(record(a->events, 1, s));
 
   HeadArgs ha;
@@ -579,7 +583,10 @@ trevs_status trevs_inllm_prune(const trevs_inllm_args* a, void* ws, size_t ws_by
   ha.lse2 = lse2;
   ha.head_var = head_var;
   TREVS_TRY(record(a->events, 2, s));
-  TREVS_HIP(launch_heads(ha, s));
+  if (a->row_stats)
+    TREVS_HIP(launch_heads_given(a->row_stats, ha, s));
+  else
+    TREVS_HIP(launch_heads(ha, s));
   TREVS_TRY(record(a->events, 3, s));
 
   ScoreArgs sa;

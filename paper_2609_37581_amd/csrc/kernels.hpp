@@ -209,6 +209,10 @@ hipError_t launch_topk(const float* scores, int B, int N, int K, int32_t* out, h
                        bool nonneg = false);
 hipError_t launch_stats(const StatsArgs& a, int dtype, int dh, hipStream_t s);
 hipError_t launch_heads(const HeadArgs& a, hipStream_t s);
+// u_h and the row log-sum-exps from the caller's per-row statistics
+// [B,H_q,T_max,3] = (log-sum-exp, sum A, sum A^2) instead of the
+// statistics pass.
+hipError_t launch_heads_given(const float* row_stats, const HeadArgs& a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs& a, int dtype, int dh, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 

@@ -290,6 +290,39 @@ __global__ __launch_bounds__(kHeadThreads) void t2v_heads_kernel(HeadArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Head pass from given row statistics, one workgroup per (head, sample): each
+// text row's log-sum-exp is taken from the caller (the layer's own attention
+// pass), converted to log2 units, and u_h of Eq. (8) is the mean over the
+// valid rows of S2/K - (S1/K)^2, with S1 and S2 the row's sum and sum of
+// squares of its attention over the visual columns.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kHeadThreads) void heads_given_kernel(const float* row_stats, HeadArgs a) {
+  __shared__ float red[kHeadThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int Tb = text_rows(a.text_len, b, a.T_max);
+  const float invK = 1.f / (float)a.K_in;
+  float vs = 0.f;
+  for (int q = tid; q < a.T_max; q += kHeadThreads) {
+    const size_t row = ((size_t)b * a.H_q + h) * a.T_max + q;
+    const float lse = row_stats[3 * row], s1 = row_stats[3 * row + 1], s2 = row_stats[3 * row + 2];
+    a.lse2[((size_t)b * a.H_q + h) * a.T_pad + q] = lse * kLog2e;
+    if (q < Tb) {
+      const float mean = s1 * invK;
+      vs += s2 * invK - mean * mean;
+    }
+  }
+  vs = wave_sum(vs);
+  if (lane == 0) red[wave] = vs;
+  __syncthreads();
+  if (tid == 0) {
+    float t = 0.f;
+    for (int w = 0; w < kHeadThreads / 64; ++w) t += red[w];
+    a.head_var[(size_t)b * a.H_q + h] = t / (float)Tb;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Token score.  A workgroup owns V = 32*VB visual tokens of one sample (tiles
 // of one sample are numbered consecutively and mapped onto one XCD, so the
 // sample's queries and keys stay in that L2).  It first ranks the heads of
@@ -653,6 +686,11 @@ hipError_t launch_stats(const StatsArgs& a, int dtype, int dh, hipStream_t s) {
 
 hipError_t launch_heads(const HeadArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(t2v_heads_kernel, dim3(a.H_q, a.B), dim3(kHeadThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_heads_given(const float* row_stats, const HeadArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(heads_given_kernel, dim3(a.H_q, a.B), dim3(kHeadThreads), 0, s, row_stats, a);
   return hipGetLastError();
 }
 

@@ -64,7 +64,7 @@ class InllmArgs(ctypes.Structure):
                 ("lse_rest", c_void_p), ("kept_idx", c_void_p), ("hidden_out", c_void_p),
                 ("k_out", c_void_p), ("v_out", c_void_p), ("pos_out", c_void_p),
                 ("head_sel", c_void_p), ("head_var", c_void_p), ("score_out", c_void_p),
-                ("events", c_void_p), ("softmax", c_int32)]
+                ("events", c_void_p), ("softmax", c_int32), ("row_stats", c_void_p)]
 
 
 class SensitivityArgs(ctypes.Structure):
@@ -280,7 +280,8 @@ class Inllm:
     """Stage 2 with outputs and workspace allocated once; call() enqueues it."""
 
     def __init__(self, q, k, v, hidden, pos, text_len=None, *, P, K_in, n_keep_heads, k_keep,
-                 scale=None, lse_rest=None, want_scores=False, softmax="visual", noalloc=False):
+                 scale=None, lse_rest=None, want_scores=False, softmax="visual", noalloc=False,
+                 row_stats=None):
         dev = hidden.device
         _check(hidden, "hidden", dev, 3)
         dt = hidden.dtype
@@ -292,6 +293,8 @@ class Inllm:
             _check(text_len, "text_len", dev, 1, torch.int32)
         if lse_rest is not None:
             _check(lse_rest, "lse_rest", dev, 3, torch.float32)
+        if row_stats is not None:
+            _check(row_stats, "row_stats", dev, 4, torch.float32)
         B, S, D = hidden.shape
         H_q, d_head = q.shape[2], q.shape[3]
         H_kv = k.shape[2]
@@ -305,8 +308,10 @@ class Inllm:
             raise ValueError("no text rows after the visual block")
         if lse_rest is not None and lse_rest.shape != (B, H_q, T_max):
             raise ValueError("lse_rest must be [B,H_q,T_max]")
+        if row_stats is not None and row_stats.shape != (B, H_q, T_max, 3):
+            raise ValueError("row_stats must be [B,H_q,T_max,3]")
         So = S - K_in + k_keep
-        self.inputs = (q, k, v, hidden, pos, text_len, lse_rest)
+        self.inputs = (q, k, v, hidden, pos, text_len, lse_rest, row_stats)
         self.kept_idx = _empty((B, k_keep), torch.int32, dev)
         self.hidden_out = _empty((B, So, D), dt, dev)
         self.k_out = _empty((B, So, H_kv, d_head), dt, dev)
@@ -327,6 +332,7 @@ class Inllm:
         a.dtype = _dtype_code(hidden)
         a.q, a.k, a.v, a.hidden, a.pos = _ptr(q), _ptr(k), _ptr(v), _ptr(hidden), _ptr(pos)
         a.text_len, a.lse_rest = _ptr(text_len), _ptr(lse_rest)
+        a.row_stats = _ptr(row_stats)
         a.softmax = SOFTMAX[softmax]
         a.kept_idx, a.hidden_out = _ptr(self.kept_idx), _ptr(self.hidden_out)
         a.k_out, a.v_out, a.pos_out = _ptr(self.k_out), _ptr(self.v_out), _ptr(self.pos_out)

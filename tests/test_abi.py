@@ -41,7 +41,7 @@ def test_every_declared_symbol_is_exported():
 def test_struct_mirror_sizes():
     L = trevs.lib()
     assert L.trevs_prellm_args_size() == ctypes.sizeof(trevs.PrellmArgs) == 168
-    assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 200
+    assert L.trevs_inllm_args_size() == ctypes.sizeof(trevs.InllmArgs) == 208
     assert L.trevs_sensitivity_args_size() == ctypes.sizeof(trevs.SensitivityArgs) == 168
 
 
@@ -237,3 +237,20 @@ def test_noalloc_rejects_on_the_host():
     need = L.trevs_inllm_workspace_size(ctypes.byref(big))
     assert need > 16 << 20
     assert L.trevs_inllm_prune_noalloc(ctypes.byref(big), None) == 3
+
+
+def test_inllm_row_stats_rejections():
+    """Caller-given row statistics exclude lse_rest, must be 4-byte aligned
+    and must not overlap an output."""
+    L = trevs.lib()
+    base = 1 << 40
+    a = _inllm(row_stats=base + (20 << 32), lse_rest=base + (21 << 32))
+    assert L.trevs_inllm_workspace_size(ctypes.byref(a)) == 0
+    a = _inllm(row_stats=base + (20 << 32) + 2)
+    assert L.trevs_inllm_workspace_size(ctypes.byref(a)) == 0
+    a = _inllm(row_stats=base + (6 << 32))  # inside hidden_out
+    assert L.trevs_inllm_workspace_size(ctypes.byref(a)) == 0
+    ok = _inllm(row_stats=base + (20 << 32))
+    plain = _inllm()
+    # no statistics pass: its split partials leave the workspace
+    assert 0 < L.trevs_inllm_workspace_size(ctypes.byref(ok)) < L.trevs_inllm_workspace_size(ctypes.byref(plain))

@@ -10,7 +10,7 @@ import oracle
 from paper_2609_37581_amd import trevs
 from parity import (assert_kept_band, assert_kept_exact_on_own_scores, assert_scores_close,
                     dev_tensor, host_bits)
-from synthetic import WORKLOADS, stage2_inputs
+from synthetic import WORKLOADS, stage2_inputs, to_storage
 
 pytestmark = pytest.mark.gpu
 
@@ -219,6 +219,94 @@ def test_stage2_identical_visual_keys_keep_the_first_tokens():
         assert np.array_equal(o["kept_idx"][b], np.arange(w.K2)), b
         rows = oracle.compaction_rows(S, w.P, w.K1, g["kept_idx"][b])
         assert np.array_equal(g["hidden_out"][b], inp["hidden"][b][rows]), b
+
+
+@pytest.mark.parametrize("scale", [0.1, 0.02])
+def test_stage2_low_contrast_heads_tied_across_the_cut(scale):
+    """Low-contrast heads (queries scaled down: per-row coefficient of
+    variation squared down to about 1e-4, where the one-pass variance of
+    Eq. (8) loses the most precision), and in each sample the last selected
+    head and the first unselected one made identical (same Q and K rows), so
+    their u_h tie exactly at the cut: the lower head index is kept."""
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=2)  # 32 MHA heads, 16 kept
+    inp = stage2_inputs(w)
+    q = oracle.to_f64(inp["q"], w.dtype) * scale
+    q_bits = to_storage(q, w.dtype)
+    o = run_oracle(dict(inp, q=q_bits), w, w.n_keep, w.K2)
+    k = inp["k"].copy()
+    for b in range(w.B):
+        order = sorted(range(w.H_q), key=lambda h: (-o["head_var"][b][h], h))
+        h_in, h_out = order[w.n_keep - 1], order[w.n_keep]
+        q_bits[b, :, h_out] = q_bits[b, :, h_in]
+        k[b, :, h_out] = k[b, :, h_in]  # MHA: KV head = query head
+    inp = dict(inp, q=q_bits, k=k)
+    print(f"[stage2] low-contrast heads x{scale}, tie at the cut", flush=True)
+    g = run_gpu(inp, w)
+    o = check(inp, w, g)
+    assert (o["head_var"] * w.K1 ** 2).min() > 5e-5  # the contrast this case covers
+    for b in range(w.B):
+        order = sorted(range(w.H_q), key=lambda h: (-o["head_var"][b][h], h))
+        h_in, h_out = order[w.n_keep - 1], order[w.n_keep]
+        assert o["head_var"][b][h_in] == o["head_var"][b][h_out], b
+        assert g["head_var"][b][h_in] == g["head_var"][b][h_out], b
+        assert min(h_in, h_out) in g["head_sel"][b] and max(h_in, h_out) not in g["head_sel"][b], b
+
+
+def _layer_row_stats(inp, w, causal):
+    """What the layer's own attention pass would hand over per text row,
+    emulated with plain float64 PyTorch on the CPU: the log-sum-exp of the
+    row's logits over its softmax domain (the visual keys, or the whole
+    causal row: prefix, visual and text keys up to the row itself, in the
+    row's KV head), and the sum and sum of squares of the resulting
+    attention over the visual columns."""
+    def f64(x):
+        return torch.from_numpy(oracle.to_f64(x, w.dtype))
+    q, k = f64(inp["q"]), f64(inp["k"])  # [B,S,H,d]
+    G = w.H_q // w.H_kv
+    k = torch.repeat_interleave(k, G, dim=2)
+    t0 = w.P + w.K1
+    qt = q[:, t0:t0 + w.T_max].permute(0, 2, 1, 3)        # [B,H,T,d]
+    kk = k.permute(0, 2, 1, 3)                             # [B,H,S,d]
+    x = (qt @ kk.transpose(-1, -2).contiguous()) / math.sqrt(w.d_h)  # [B,H,T,S]
+    keys = torch.arange(w.S)
+    if causal:
+        allowed = keys[None, :] <= (t0 + torch.arange(w.T_max))[:, None]
+    else:
+        allowed = (keys[None, :] >= w.P) & (keys[None, :] < t0) & torch.ones(w.T_max, 1, dtype=torch.bool)
+    x = x.masked_fill(~allowed, float("-inf"))
+    lse = torch.logsumexp(x, dim=-1)
+    A = torch.exp(x[..., w.P:t0] - lse[..., None])
+    out = torch.stack([lse, A.sum(-1), (A * A).sum(-1)], dim=-1)
+    return out.to(torch.float32).contiguous()
+
+
+@pytest.mark.parametrize("name,causal", [("qwen25vl-b1", True), ("llava15-b3", True),
+                                         ("llava15-b3", False), ("gqa-dh64-ragged", True)])
+def test_stage2_row_stats_from_the_layer(name, causal):
+    """Stage 2 fed the per-row statistics of the layer's own attention pass
+    (no statistics pass in the library): u_h, H*, p, the kept set and the
+    compaction against the oracle's full computation in the same softmax
+    domain."""
+    w = {"qwen25vl-b1": WORKLOADS["qwen25vl-b4-bf16"].with_(B=1),
+         "llava15-b3": WORKLOADS["llava15-b64-bf16"].with_(B=3),
+         "gqa-dh64-ragged": CASES["ragged-bf16-dh64"]}[name]
+    softmax = "causal" if causal else "visual"
+    print(f"[stage2] row statistics from the layer: {name} {softmax}", flush=True)
+    inp = stage2_inputs(w)
+    rs = _layer_row_stats(inp, w, causal)
+    q = dev_tensor(inp["q"], w.dtype)
+    k = dev_tensor(inp["k"], w.dtype)
+    call = trevs.Inllm(q, k, dev_tensor(inp["v"], w.dtype), dev_tensor(inp["hidden"], w.dtype),
+                       torch.from_numpy(inp["pos"]).cuda(), torch.from_numpy(inp["text_len"]).cuda(),
+                       P=w.P, K_in=w.K1, n_keep_heads=w.n_keep, k_keep=w.K2, want_scores=True,
+                       row_stats=rs.cuda())
+    call()
+    torch.cuda.synchronize()
+    g = dict(kept_idx=call.kept_idx.cpu().numpy(), hidden_out=host_bits(call.hidden_out),
+             k_out=host_bits(call.k_out), v_out=host_bits(call.v_out), pos_out=call.pos_out.cpu().numpy(),
+             head_sel=call.head_sel.cpu().numpy(), head_var=call.head_var.cpu().numpy(),
+             score=call.score.cpu().numpy())
+    check(inp, w, g, softmax=softmax)
 
 
 def test_stage2_text_lengths_out_of_range_are_clamped():
