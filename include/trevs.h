@@ -84,7 +84,10 @@ typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
  * preservation, Sec. 4.1 after Eq. (7)): one at a time, the token outside
  * the selected set whose cosine distance 1 - zbar_i . zbar_j to its nearest
  * selected token is largest (ties to the lower index).  This forms the Gram
- * matrix Z Z^T of every sample in the workspace (B*N*N floats).
+ * matrix Z Z^T of every sample in the workspace (B*N*N floats beyond the
+ * k_div = 0 size, e.g. 4.3 GB at B = 4, N = 16,384; 85 MB at B = 64,
+ * N = 576); trevs_prellm_workspace_size includes it, and the call itself
+ * allocates nothing.
  * With ratio_mode = TREVS_RATIO_BUDGET the textual ratio is instead the
  * share of the token budget given to textual relevance (the reading of the
  * preliminary analysis, Sec. 3): K_t = floor(rho * k_keep + 1/2) tokens with
