@@ -24,7 +24,10 @@ namespace trevs {
 // cores, each a 64x64 block.  Bytes past a row's end (a partial last slab)
 // load as zero.  The tile is written in place and, off the diagonal, also
 // transposed through LDS (rows padded to 129 floats) with coalesced stores.
-// Diagonal tiles also write 1/max(||z_i||, 1e-12) from G_ii.
+// Diagonal tiles also write 1/max(||z_i||, 1e-12) from G_ii.  G is written
+// with nontemporal stores: the picks read it back long after it has left the
+// caches, and cached stores would evict operand slabs the other resident
+// workgroups still read.
 // ---------------------------------------------------------------------------
 constexpr int kGramTile = 128;
 constexpr int kGramThreads = 256;
@@ -72,6 +75,7 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   if (tj > ti || ti >= nT) return;  // the whole workgroup: no barrier has run
   const int N = a.N, rb = a.row_bytes;
   const int n_slabs = (rb + 127) / 128;
+  const int tail = rb & 127;  // bytes of a partial last slab, 0 if none
   const uint8_t* zb = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
   const int cr = tid >> 3, cc = tid & 7;
   const uint8_t* src[2 * VPT];  // row starts (rows past N re-read row N - 1)
@@ -84,22 +88,28 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   const int sdst = cr * 128 + gram_swizzle(cr, cc) * 16;  // rows 32 apart share the swizzle
   u32x4 g[2][2 * VPT];
   // chunk cc of slab s; a chunk past the row's end reads the row's first
-  // chunk (in bounds) and is replaced by zero; the padding steps past the
-  // last slab re-read it and are never multiplied
+  // chunk (in bounds), and the store overwrites its LDS copy with zeros (a
+  // select on the loaded vectors made the compiler wait for every load in
+  // flight at the top of each iteration); the padding steps past the last
+  // slab re-read it and are never multiplied
   auto load = [&](int s, u32x4 (&dst)[2 * VPT]) {
     const int off = min(s, n_slabs - 1) * 128 + cc * 16;
-    const bool in_row = off < rb;
+    const int o = off < rb ? off : 0;
 #pragma unroll
-    for (int k = 0; k < 2 * VPT; ++k) {
-      const u32x4 v = ldg16(src[k] + (in_row ? off : 0));
-      dst[k] = in_row ? v : zero4();
-    }
+    for (int k = 0; k < 2 * VPT; ++k) dst[k] = ldg16(src[k] + o);
   };
-  auto store = [&](uint8_t* st, const u32x4 (&v)[2 * VPT]) {
+  auto store = [&](uint8_t* st, const u32x4 (&v)[2 * VPT], int s) {
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
       *reinterpret_cast<u32x4*>(st + sdst + k * (kGramThreads / 8) * 128) = v[k];
       *reinterpret_cast<u32x4*>(st + SLAB + sdst + k * (kGramThreads / 8) * 128) = v[VPT + k];
+    }
+    if (s == n_slabs - 1 && tail && cc * 16 >= tail) {  // chunks past the row's end hold zeros
+#pragma unroll
+      for (int k = 0; k < VPT; ++k) {
+        *reinterpret_cast<u32x4*>(st + sdst + k * (kGramThreads / 8) * 128) = zero4();
+        *reinterpret_cast<u32x4*>(st + SLAB + sdst + k * (kGramThreads / 8) * 128) = zero4();
+      }
     }
   };
   const int wj = wave >> 1, wi = wave & 1;
@@ -126,7 +136,10 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
 #pragma unroll
       for (int n = 0; n < 2; ++n) acc[m][n] = mfma_frag(fa[m], fb[n], acc[m][n], In{});
   };
+  // stage 0's loads go out first: loads complete in order, so the first
+  // store then waits only for them, not for stage 1's as well
   load(0, g[0]);
+  __builtin_amdgcn_sched_barrier(0);
   load(1, g[1]);
   const int n_iter = (n_slabs + 1) / 2;
   for (int it = 0; it < n_iter; ++it) {
@@ -136,7 +149,7 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
       uint8_t* st = c ? l1 : l0;
       // buffer c was last read at step s - 2, before every wave passed the
       // barrier of step s - 1
-      store(st, g[c]);
+      store(st, g[c], s);
       load(s + 2, g[c]);
       __syncthreads();
       if (s < n_slabs) compute(st);
@@ -153,7 +166,7 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = tj * T + wj * 64 + m * 32 + mfma_row(r, half);
-        if (i < N && j < N) gb[(size_t)j * N + i] = acc[m][n][r];
+        if (i < N && j < N) __builtin_nontemporal_store(acc[m][n][r], &gb[(size_t)j * N + i]);
       }
     }
   if (tj == ti) {  // the diagonal tile holds ||z_i||^2
@@ -185,7 +198,7 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   for (int e = tid; e < T * T; e += kGramThreads) {
     const int il = e / T, jl = e - il * T;
     const int i = ti * T + il, j = tj * T + jl;
-    if (i < N && j < N) gb[(size_t)i * N + j] = tile[jl * TP + il];
+    if (i < N && j < N) __builtin_nontemporal_store(tile[jl * TP + il], &gb[(size_t)i * N + j]);
   }
 }
 
@@ -230,6 +243,7 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
   if (tj > ti || ti >= nT) return;  // the whole workgroup: no barrier has run
   const int N = a.N, rb = a.row_bytes;
   const int n_slabs = (rb + 127) / 128;
+  const int tail = rb & 127;  // bytes of a partial last slab, 0 if none
   const uint8_t* zb = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
   const int cr = tid >> 3, cc = tid & 7;
   const uint8_t* src[2 * VPT];  // row starts (rows past N re-read row N - 1)
@@ -243,18 +257,22 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
   u32x4 g[2][2 * VPT];
   auto load = [&](int s, u32x4 (&dst)[2 * VPT]) {
     const int off = min(s, n_slabs - 1) * 128 + cc * 16;
-    const bool in_row = off < rb;
+    const int o = off < rb ? off : 0;
 #pragma unroll
-    for (int k = 0; k < 2 * VPT; ++k) {
-      const u32x4 v = ldg16(src[k] + (in_row ? off : 0));
-      dst[k] = in_row ? v : zero4();
-    }
+    for (int k = 0; k < 2 * VPT; ++k) dst[k] = ldg16(src[k] + o);
   };
-  auto store = [&](uint8_t* st, const u32x4 (&v)[2 * VPT]) {
+  auto store = [&](uint8_t* st, const u32x4 (&v)[2 * VPT], int s) {
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
       *reinterpret_cast<u32x4*>(st + sdst + k * (kGram256Threads / 8) * 128) = v[k];
       *reinterpret_cast<u32x4*>(st + SLAB + sdst + k * (kGram256Threads / 8) * 128) = v[VPT + k];
+    }
+    if (s == n_slabs - 1 && tail && cc * 16 >= tail) {  // chunks past the row's end hold zeros
+#pragma unroll
+      for (int k = 0; k < VPT; ++k) {
+        *reinterpret_cast<u32x4*>(st + sdst + k * (kGram256Threads / 8) * 128) = zero4();
+        *reinterpret_cast<u32x4*>(st + SLAB + sdst + k * (kGram256Threads / 8) * 128) = zero4();
+      }
     }
   };
   const int wj = wave >> 2, wi = wave & 3;  // rows wj*128.., columns wi*64.. of the tile
@@ -285,7 +303,10 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
         for (int n = 0; n < 2; ++n) acc[m][n] = mfma_frag(fa[m], fb[n], acc[m][n], In{});
     }
   };
+  // stage 0's loads go out first: loads complete in order, so the first
+  // store then waits only for them, not for stage 1's as well
   load(0, g[0]);
+  __builtin_amdgcn_sched_barrier(0);
   load(1, g[1]);
   const int n_iter = (n_slabs + 1) / 2;
   for (int it = 0; it < n_iter; ++it) {
@@ -295,7 +316,7 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
       uint8_t* st = c ? l1 : l0;
       // buffer c was last read at step s - 2, before every wave passed the
       // barrier of step s - 1
-      store(st, g[c]);
+      store(st, g[c], s);
       load(s + 2, g[c]);
       __syncthreads();
       if (s < n_slabs) compute(st);
@@ -312,7 +333,7 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = tj * T + wj * 128 + m * 32 + mfma_row(r, half);
-        if (i < N && j < N) gbm[(size_t)j * N + i] = acc[m][n][r];
+        if (i < N && j < N) __builtin_nontemporal_store(acc[m][n][r], &gbm[(size_t)j * N + i]);
       }
     }
   if (tj == ti) {  // the diagonal tile holds ||z_i||^2
@@ -351,7 +372,7 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
     for (int e = tid; e < T * 64; e += kGram256Threads) {
       const int il = e >> 6, jl = e & 63;
       const int i = ti * T + il, j = tj * T + 64 * p + jl;
-      if (i < N && j < N) gbm[(size_t)i * N + j] = tile[jl * TP + il];
+      if (i < N && j < N) __builtin_nontemporal_store(tile[jl * TP + il], &gbm[(size_t)i * N + j]);
     }
   }
 }

@@ -300,6 +300,12 @@ FPS_CASES = {
     "gram256-ragged-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
         B=2, N=2500, d=520, K1=300, n_sal=8, n_qm=10), 100),
     "gram256-f32": (WORKLOADS["llava15-b1-f32"].with_(N=2100, d=256, K1=200), 60),
+    # whole 256-row tiles (N = 4096, two super-blocks a side), and a last
+    # slab of 64 of 128 bytes (zeroed in LDS) with N not a multiple of 4
+    "gram256-whole-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=2, N=4096, d=1024, K1=512, n_sal=8, n_qm=10), 128),
+    "gram256-tail64-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=2, N=2310, d=544, K1=300, n_sal=8, n_qm=10), 100),
 }
 
 
