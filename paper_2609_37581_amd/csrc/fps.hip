@@ -456,43 +456,53 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
     const int i = e * kSelThreads + tid;
     if (valid(e) && ((pivbits[i >> 5] >> (i & 31)) & 1u)) sel |= 1u << e;
   }
+  // selected and padding elements hold distance -inf: they never win a step,
+  // and the row updates (a minimum) keep them there, so neither the argmax
+  // nor the update tests them
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (!valid(e) || ((sel >> e) & 1u)) dist[e] = -INFINITY;
   for (int t = 0; t < a.K_d; ++t) {
     float v = -INFINITY;
-    int idx = 0x7fffffff;
+    uint32_t idx = 0xffffffffu;
 #pragma unroll
     for (int e = 0; e < E; ++e)
-      if (valid(e) && !((sel >> e) & 1u) && dist[e] > v) {  // ascending e: the lower index wins ties
+      if (dist[e] > v) {  // ascending e: the lower index wins ties
         v = dist[e];
-        idx = e * kSelThreads + tid;
+        idx = (uint32_t)(e * kSelThreads + tid);
       }
     const float vm = wave_max(v);
-    const uint32_t im = wave_min_u32(v == vm ? (uint32_t)idx : 0xffffffffu);
+    const uint32_t im = wave_min_u32(v == vm ? idx : 0xffffffffu);
     const int buf = t & 1;  // alternate slots: one barrier per step suffices
     if (lane == 0) {
       wv[buf][wave] = vm;
       wi[buf][wave] = (int)im;
     }
     __syncthreads();
-    float bv = wv[buf][0];
-    int w = wi[buf][0];
-#pragma unroll
-    for (int k = 1; k < kSelWaves; ++k) {
-      const float v2 = wv[buf][k];
-      const int i2 = wi[buf][k];
-      if (v2 > bv || (v2 == bv && i2 < w)) {
-        bv = v2;
-        w = i2;
-      }
-    }
+    // every wave reduces the waves' winners itself (distance desc, index asc)
+    const float v2 = lane < kSelWaves ? wv[buf][lane] : -INFINITY;
+    const uint32_t i2 = lane < kSelWaves ? (uint32_t)wi[buf][lane] : 0xffffffffu;
+    const float bv = wave_max(v2);
+    int w = (int)wave_min_u32(v2 == bv ? i2 : 0xffffffffu);
     w = min(max(w, 0), N - 1);  // K_r + K_d <= N leaves a candidate at every step
     if (tid == 0 && a.div_idx) a.div_idx[(size_t)b * a.K_d + t] = w;
-    if ((w & (kSelThreads - 1)) == tid) sel |= 1u << (w / kSelThreads);
+    const int we = w / kSelThreads;
+    const bool mine = (w & (kSelThreads - 1)) == tid;
+    if (mine) sel |= 1u << we;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (mine && e == we) dist[e] = -INFINITY;
     const float* row = gb + (size_t)w * N;
     const float izw = a.inv_norm[(size_t)b * N + w];
+    // all of the row's loads go out before any is used (one round trip)
+    float gi[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) gi[e] = row[min(e * kSelThreads + tid, N - 1)];
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const float gi = row[min(e * kSelThreads + tid, N - 1)];
-      if (valid(e) && !((sel >> e) & 1u)) dist[e] = fminf(dist[e], 1.f - gi * iz[e] * izw);
+      const float d = 1.f - gi[e] * iz[e] * izw;
+      dist[e] = d < dist[e] ? d : dist[e];
     }
   }
   block_write_mask<E>(sel, K_r + a.K_d, a.kept_idx + (size_t)b * (K_r + a.K_d), sh);
