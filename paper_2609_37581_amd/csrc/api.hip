@@ -131,7 +131,7 @@ PrellmLayout prellm_layout(const trevs_prellm_args* a) {
     L.gram = off;
     off = align_up(off + (size_t)a->B * a->N * a->N * sizeof(float));
     L.dist = off;
-    off = align_up(off + (size_t)a->B * a->N * sizeof(float));
+    off = align_up(off + (size_t)fps_init_splits(a->k_keep - a->k_div) * a->B * a->N * sizeof(float));
     L.inv_norm = off;
     off = align_up(off + (size_t)a->B * a->N * sizeof(float));
   }
@@ -504,6 +504,8 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
     fa.N = a->N;
     fa.K_r = K_r;
     fa.K_d = a->k_div;
+    fa.B = a->B;
+    fa.n_psplit = fps_init_splits(K_r);
     fa.dist = reinterpret_cast<float*>(w + L.dist);
     fa.inv_norm = reinterpret_cast<float*>(w + L.inv_norm);
     fa.kept_idx = a->kept_idx;

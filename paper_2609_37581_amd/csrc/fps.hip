@@ -380,22 +380,27 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
 // ---------------------------------------------------------------------------
 // Initial distances: for every token i, 1 - max over the pivots j of
 // cos(z_i, z_j) = G_ij / (||z_i|| ||z_j||), with the inverse norms the Gram
-// pass wrote.  One thread per token; the pivot loop is unrolled so that
-// several row reads of G are in flight (a pivot's row is read at consecutive
-// columns by consecutive threads).
+// pass wrote.  One thread per token; the pivots are split over n_psplit
+// workgroups per token block (grid z), each writing the maximum of
+// G_ij / ||z_j|| over its share; the picks kernel takes the maximum over the
+// splits (exact, so the order does not matter) and forms the distance.  The
+// pivot loop is unrolled so that several row reads of G are in flight (a
+// pivot's row is read at consecutive columns by consecutive threads).
 // ---------------------------------------------------------------------------
 constexpr int kFpsInitThreads = 256;
 
 __global__ __launch_bounds__(kFpsInitThreads) void fps_init_kernel(FpsArgs a) {
-  const int b = blockIdx.y, N = a.N;
+  const int b = blockIdx.y, split = blockIdx.z, N = a.N;
   const int i = min((int)(blockIdx.x * kFpsInitThreads + threadIdx.x), N - 1);
   const float* gb = a.G + (size_t)b * N * N;
   const float* inb = a.inv_norm + (size_t)b * N;
+  const int per = (a.K_r + a.n_psplit - 1) / a.n_psplit;
+  const int p_begin = min(split * per, a.K_r), p_end = min(p_begin + per, a.K_r);
   const int32_t* piv = a.pivots + (size_t)b * a.K_r;
   constexpr int U = 8;
   float mx = -INFINITY;
-  int p = 0;
-  for (; p + U <= a.K_r; p += U) {
+  int p = p_begin;
+  for (; p + U <= p_end; p += U) {
     int j[U];
     float g[U], izj[U];
 #pragma unroll
@@ -408,11 +413,11 @@ __global__ __launch_bounds__(kFpsInitThreads) void fps_init_kernel(FpsArgs a) {
 #pragma unroll
     for (int u = 0; u < U; ++u) mx = fmaxf(mx, g[u] * izj[u]);
   }
-  for (; p < a.K_r; ++p) {
+  for (; p < p_end; ++p) {
     const int j = piv[p];
     mx = fmaxf(mx, gb[(size_t)j * N + i] * inb[j]);
   }
-  if (blockIdx.x * kFpsInitThreads + threadIdx.x < N) a.dist[(size_t)b * N + i] = 1.f - mx * inb[i];
+  if (blockIdx.x * kFpsInitThreads + threadIdx.x < N) a.dist[((size_t)split * a.B + b) * N + i] = mx;
 }
 
 // ---------------------------------------------------------------------------
@@ -441,8 +446,10 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int i = min(e * kSelThreads + tid, N - 1);
-    dist[e] = a.dist[(size_t)b * N + i];
+    float mx = a.dist[(size_t)b * N + i];
+    for (int sp = 1; sp < a.n_psplit; ++sp) mx = fmaxf(mx, a.dist[((size_t)sp * a.B + b) * N + i]);
     iz[e] = a.inv_norm[(size_t)b * N + i];
+    dist[e] = 1.f - mx * iz[e];
   }
   __syncthreads();
   for (int p = tid; p < K_r; p += kSelThreads) {
@@ -525,7 +532,7 @@ hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hip
     else
       hipLaunchKernelGGL(gram_kernel<F32>, ggrid, dim3(kGramThreads), 0, s, g);
   }
-  hipLaunchKernelGGL(fps_init_kernel, dim3((f.N + kFpsInitThreads - 1) / kFpsInitThreads, B),
+  hipLaunchKernelGGL(fps_init_kernel, dim3((f.N + kFpsInitThreads - 1) / kFpsInitThreads, B, f.n_psplit),
                      dim3(kFpsInitThreads), 0, s, f);
   const int E = select_e(f.N);
 #define CALL(E_) hipLaunchKernelGGL(fps_pick_kernel<E_>, dim3(B), dim3(kSelThreads), 0, s, f)

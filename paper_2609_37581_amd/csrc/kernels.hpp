@@ -125,13 +125,21 @@ struct FpsArgs {
   const float* G;            // [B,N,N]
   const int32_t* pivots;     // [B,K_r] ascending
   int N, K_r, K_d;
-  float* dist;               // [B,N] work: distance to the selected set
+  int B;
+  int n_psplit;              // pivot splits of the initial distances (fps_init_splits)
+  float* dist;               // [n_psplit,B,N] work: per split, max over its pivots j of G_ij / ||z_j||
   float* inv_norm;           // [B,N] work: 1 / max(||z_i||, 1e-12), from the Gram pass
   int32_t* kept_idx;         // [B,K_r+K_d] ascending
   int32_t* div_idx;          // [B,K_d] picks in pick order, or null
 };
 // Gram matrix, initial distances and the K_d sequential picks.
 hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hipStream_t s);
+// Pivot splits of the initial-distance pass (workgroups per token block):
+// about 256 pivots each, at most 8.
+inline int fps_init_splits(int K_r) {
+  const int s = K_r / 256;
+  return s < 1 ? 1 : (s > 8 ? 8 : s);
+}
 
 // ---------------------------------------------------------------- analysis
 struct ProfileArgs {
