@@ -58,7 +58,8 @@ typedef enum trevs_status {
 typedef enum trevs_dtype { TREVS_F32 = 0, TREVS_BF16 = 1 } trevs_dtype;
 
 /* Implementation limits (TREVS_ERR_UNSUPPORTED beyond them). */
-#define TREVS_MAX_SELECT_N 32768 /* tokens ranked per sample by one top-K */
+#define TREVS_MAX_SELECT_N 65536 /* tokens ranked per sample by one top-K */
+#define TREVS_MAX_FPS_N 32768    /* tokens per sample with a diversity set (k_div > 0) */
 #define TREVS_PRELLM_NUM_KERNELS 5 /* prep, relevance, robust stats, fuse+top-K (+ diversity set), gather */
 #define TREVS_INLLM_NUM_KERNELS 5  /* t2v stats (+ causal rest keys), head variance, head set+token score, top-K, compaction */
 #define TREVS_SENSITIVITY_NUM_KERNELS 7 /* per question: t2v stats, head variance, profile; then Eq. (1) */
@@ -109,7 +110,7 @@ typedef struct trevs_prellm_args {
   int32_t d;                 /* projected width d'; d * elem_size % 16 == 0 */
   int32_t M_max;             /* padded text rows, >= 1 */
   int32_t k_keep;            /* K_1 = K_r + K_d, 1..N */
-  int32_t k_div;             /* K_d farthest-point diversity tokens, 0..k_keep-1 */
+  int32_t k_div;             /* K_d farthest-point diversity tokens, 0..k_keep-1; N <= TREVS_MAX_FPS_N when > 0 */
   float textual_ratio;       /* rho in [0, 1]; 0.5 reproduces Eq. (7) */
   float tau_v, tau_t;        /* temperatures > 0 (paper: 1.4, 1.0) */
   float lambda_;             /* consistency reward weight >= 0 (paper: 1.0) */

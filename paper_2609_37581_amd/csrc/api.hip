@@ -99,6 +99,7 @@ trevs_status validate_prellm(const trevs_prellm_args* a) {
   if (a->ratio_mode != TREVS_RATIO_WEIGHTS && a->ratio_mode != TREVS_RATIO_BUDGET) return TREVS_ERR_INVALID_ARG;
   if (a->ratio_mode == TREVS_RATIO_BUDGET && (a->score_out || a->norm_stats)) return TREVS_ERR_INVALID_ARG;
   if (a->N > TREVS_MAX_SELECT_N) return TREVS_ERR_UNSUPPORTED;
+  if (a->k_div > 0 && a->N > TREVS_MAX_FPS_N) return TREVS_ERR_UNSUPPORTED;
   return TREVS_OK;
 }
 

@@ -170,6 +170,18 @@ __device__ __forceinline__ int wave_incl_scan(int v, int /*lane*/) {
   return v;
 }
 
+// The same inclusive scan in unsigned (wrapping) arithmetic.
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
+  auto add = [](uint32_t a, int b) { return a + (uint32_t)b; };
+  v = add(v, dpp::mov<dpp::kShr1>(0, (int)v));
+  v = add(v, dpp::mov<dpp::kShr2>(0, (int)v));
+  v = add(v, dpp::mov<dpp::kShr4>(0, (int)v));
+  v = add(v, dpp::mov<dpp::kShr8>(0, (int)v));
+  v = add(v, dpp::mov<dpp::kBcast15, 0xa>(0, (int)v));
+  v = add(v, dpp::mov<dpp::kBcast31, 0xc>(0, (int)v));
+  return v;
+}
+
 // Order-preserving map from fp32 to uint32 (-0 taken as +0).
 __device__ __forceinline__ uint32_t f2key(float f) {
   const uint32_t u = __float_as_uint(f + 0.0f);  // -0 + +0 is +0: both zeros share one key

@@ -457,11 +457,11 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
     atomicOr(&pivbits[j >> 5], 1u << (j & 31));
   }
   __syncthreads();
-  uint32_t sel = 0u;  // bit e: element e is selected (a pivot or a pick)
+  SelMask<E> sel = 0;  // bit e: element e is selected (a pivot or a pick)
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int i = e * kSelThreads + tid;
-    if (valid(e) && ((pivbits[i >> 5] >> (i & 31)) & 1u)) sel |= 1u << e;
+    if (valid(e) && ((pivbits[i >> 5] >> (i & 31)) & 1u)) sel |= SelMask<E>(1) << e;
   }
   // selected and padding elements hold distance -inf: they never win a step,
   // and the row updates (a minimum) keep them there, so neither the argmax
@@ -495,7 +495,7 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
     if (tid == 0 && a.div_idx) a.div_idx[(size_t)b * a.K_d + t] = w;
     const int we = w / kSelThreads;
     const bool mine = (w & (kSelThreads - 1)) == tid;
-    if (mine) sel |= 1u << we;
+    if (mine) sel |= SelMask<E>(1) << we;
 #pragma unroll
     for (int e = 0; e < E; ++e)
       if (mine && e == we) dist[e] = -INFINITY;

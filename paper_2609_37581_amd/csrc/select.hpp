@@ -3,6 +3,8 @@
 // (element e*1024 + t is its e-th), so loads and stores are coalesced.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace trevs {
@@ -14,12 +16,16 @@ constexpr int kFirstBins = 1 << kFirstBits;
 constexpr int kLaterBits = 8;                 // digit width of the candidate passes
 constexpr int kCandCap = 4096;                // candidates kept in LDS after the first pass
 
-constexpr int kMaxE = 32;                     // elements per thread (N <= 32768)
+constexpr int kMaxE = 64;                     // elements per thread (N <= 65536)
+
+// One bit per element of a thread (bit e: element e*1024 + t).
+template <int E>
+using SelMask = typename std::conditional<(E > 32), uint64_t, uint32_t>::type;
 
 struct SelectShared {
   uint32_t hist[kFirstBins];
   uint32_t cand[kCandCap];
-  int wcnt[kMaxE * kSelWaves];                // per (element round, wave) counts
+  uint32_t wcnt[kMaxE * kSelWaves];           // per (element round, wave) counts
   uint32_t mn[kSelWaves];
   uint32_t mx[kSelWaves];
   int wave_tot[kSelWaves];
@@ -274,19 +280,22 @@ __device__ void block_select(KeyF keyf, int N, int rank, uint32_t& res, int& les
 
 // Exclusive prefix sums of sh.wcnt[0, n) in place (n <= kMaxE * kSelWaves),
 // by wave 0; entries are ordered (element round, wave), which is index order.
+// Unsigned (wrapping) sums: packed entries carry a count in each 16-bit
+// half, and only the exclusive sums, which stay below 2^16 in each half,
+// are read.
 __device__ __forceinline__ void wcnt_scan(int n, SelectShared& sh) {
   __syncthreads();
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
     const int per = (n + kWave - 1) / kWave;
-    int* c = sh.wcnt + lane * per;
-    int lsum = 0;
+    uint32_t* c = sh.wcnt + lane * per;
+    uint32_t lsum = 0u;
     for (int j = 0; j < per; ++j)
       if (lane * per + j < n) lsum += c[j];
-    int run = wave_incl_scan(lsum, lane) - lsum;
+    uint32_t run = wave_incl_scan_u32(lsum) - lsum;
     for (int j = 0; j < per; ++j)
       if (lane * per + j < n) {
-        const int v = c[j];
+        const uint32_t v = c[j];
         c[j] = run;
         run += v;
       }
@@ -298,15 +307,15 @@ __device__ __forceinline__ void wcnt_scan(int n, SelectShared& sh) {
 // element e is kept, i.e. its key is above the K-th largest, or equal to it
 // and among the lowest-index elements of that key (K in 0..N).
 template <int E, class KeyF>
-__device__ uint32_t block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
+__device__ SelMask<E> block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int nv = thread_rounds<E>(N);
   auto valid = [&](int e) { return e < nv; };
-  if (K <= 0) return 0u;
+  if (K <= 0) return SelMask<E>(0);
   if (K >= N) {
-    uint32_t all = 0u;
+    SelMask<E> all = 0;
 #pragma unroll
-    for (int e = 0; e < E; ++e) all |= valid(e) ? (1u << e) : 0u;
+    for (int e = 0; e < E; ++e) all |= valid(e) ? (SelMask<E>(1) << e) : SelMask<E>(0);
     return all;
   }
   uint32_t key[E];
@@ -329,13 +338,13 @@ __device__ uint32_t block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
     if (lane == 0) sh.wcnt[e * kSelWaves + wave] = __popcll(bal);
   }
   wcnt_scan(E * kSelWaves, sh);
-  uint32_t keep_mask = 0u;
+  SelMask<E> keep_mask = 0;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const bool eqe = is_eq(e);
-    const int eq_rank = sh.wcnt[e * kSelWaves + wave] + lanes_below(__ballot(eqe));
+    const int eq_rank = (int)sh.wcnt[e * kSelWaves + wave] + lanes_below(__ballot(eqe));
     const bool keep = valid(e) && (key[e] > thr || (eqe && eq_rank < need_eq));
-    keep_mask |= keep ? (1u << e) : 0u;
+    keep_mask |= keep ? (SelMask<E>(1) << e) : SelMask<E>(0);
   }
   __syncthreads();  // sh.wcnt is rewritten by the caller's next step
   return keep_mask;
@@ -344,7 +353,7 @@ __device__ uint32_t block_topk_mask(KeyF keyf, int N, int K, SelectShared& sh) {
 // Writes the indices of the elements set in `mask` (K of them over the
 // workgroup) in ascending order to out[0..K).
 template <int E>
-__device__ void block_write_mask(uint32_t mask, int K, int32_t* out, SelectShared& sh) {
+__device__ void block_write_mask(SelMask<E> mask, int K, int32_t* out, SelectShared& sh) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   auto lanes_below = [&](unsigned long long bal) {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
@@ -359,7 +368,7 @@ __device__ void block_write_mask(uint32_t mask, int K, int32_t* out, SelectShare
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const bool kp = (mask >> e) & 1u;
-    const int pos = sh.wcnt[e * kSelWaves + wave] + lanes_below(__ballot(kp));
+    const int pos = (int)sh.wcnt[e * kSelWaves + wave] + lanes_below(__ballot(kp));
     if (kp && pos < K) out[pos] = e * kSelThreads + tid;  // exactly K kept; the bound guards memory
   }
 }
@@ -370,7 +379,8 @@ __device__ void block_write_mask(uint32_t mask, int K, int32_t* out, SelectShare
 // the rest: element i goes to slot above(i) + min(ties(i), need), where
 // above(i) and ties(i) count the elements before i (in index order) above the
 // threshold and equal to it, and need is how many ties are kept.  The two
-// counts travel packed in one int (low and high 16 bits; N <= 32768).
+// counts travel packed in one word (low and high 16 bits: every exclusive
+// count is below N <= 65536).
 // have_range, kmin, kmax: bounds of the keys, as for block_select.
 template <int E>
 __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* out,
@@ -402,7 +412,7 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
     const uint32_t k = key[e];
     const unsigned long long ba = __ballot(valid(e) && k > thr);
     const unsigned long long bt = __ballot(valid(e) && k == thr);
-    if (lane == 0) sh.wcnt[e * kSelWaves + wave] = __popcll(ba) | (__popcll(bt) << 16);
+    if (lane == 0) sh.wcnt[e * kSelWaves + wave] = (uint32_t)__popcll(ba) | ((uint32_t)__popcll(bt) << 16);
   }
   wcnt_scan(E * kSelWaves, sh);
   // the output base lives in a VGPR pair: held in SGPRs through the
@@ -416,9 +426,9 @@ __device__ void block_topk_write(const float (&sc)[E], int N, int K, int32_t* ou
     const bool above = valid(e) && k > thr, tie = valid(e) && k == thr;
     const unsigned long long ba = __ballot(above);
     const unsigned long long bt = __ballot(tie);
-    const int base = sh.wcnt[e * kSelWaves + wave];
-    const int na = (base & 0xffff) + lanes_below(ba);  // above the threshold, before this element
-    const int nt = (base >> 16) + lanes_below(bt);     // ties before this element
+    const uint32_t base = sh.wcnt[e * kSelWaves + wave];
+    const int na = (int)(base & 0xffffu) + lanes_below(ba);  // above the threshold, before this element
+    const int nt = (int)(base >> 16) + lanes_below(bt);      // ties before this element
     if (above || (tie && nt < need)) {
       const int pos = na + min(nt, need);
       if (pos < K) o[pos] = e * kSelThreads + tid;  // exactly K kept; the bound guards memory

@@ -741,8 +741,8 @@ __global__ __launch_bounds__(kSelThreads) void budget_topk_kernel(SelArgs a) {
     sv[e] = a.sal[(size_t)b * N + i];
     st[e] = a.rel[(size_t)b * N + i];
   }
-  const uint32_t by_text = block_topk_mask<E>([&](int e) { return f2key(st[e]); }, N, a.K_t, sh);
-  const uint32_t by_sal = block_topk_mask<E>(
+  const SelMask<E> by_text = block_topk_mask<E>([&](int e) { return f2key(st[e]); }, N, a.K_t, sh);
+  const SelMask<E> by_sal = block_topk_mask<E>(
       [&](int e) { return (by_text >> e) & 1u ? 0u : f2key(sv[e]); }, N, a.K - a.K_t, sh);
   block_write_mask<E>(by_text | by_sal, a.K, a.kept_idx + (size_t)b * a.K, sh);
 }
@@ -908,6 +908,7 @@ hipError_t launch_relevance(const RelArgs& a, const RelPlan& p, int dtype, hipSt
     case 8: CALL(8); break;             \
     case 16: CALL(16); break;           \
     case 32: CALL(32); break;           \
+    case 64: CALL(64); break;           \
     default: return hipErrorInvalidValue; \
   }
 

@@ -18,7 +18,8 @@ TREVS_F32, TREVS_BF16 = 0, 1
 PRELLM_NUM_KERNELS = 5
 INLLM_NUM_KERNELS = 5
 SENSITIVITY_NUM_KERNELS = 7
-MAX_SELECT_N = 32768
+MAX_SELECT_N = 65536
+MAX_FPS_N = 32768
 PRELLM_KERNELS = ("prep", "relevance", "norm_stats", "fuse_topk", "gather")
 INLLM_KERNELS = ("t2v_stats", "head_var", "token_score", "topk", "compaction")
 SENSITIVITY_KERNELS = ("t2v_stats.0", "head_var.0", "profile.0", "t2v_stats.1", "head_var.1",

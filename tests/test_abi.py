@@ -121,7 +121,8 @@ def test_small_grids_reserve_split_partials():
     (dict(eps=-1.0), 1), (dict(dtype=7), 1), (dict(vis_feats=None), 1),
     (dict(kept_feats=(1 << 40) + 8), 1), (dict(struct_size=10), 1), (dict(k_div=192), 1),
     (dict(k_div=-1), 1), (dict(k_div=3, div_idx=(1 << 40) + (5 << 32) + 2), 1),
-    (dict(N=40000, k_keep=10, n_seg=1), 2),
+    (dict(N=70000, k_keep=10, n_seg=1), 2),
+    (dict(N=40000, k_keep=10, n_seg=1, k_div=3), 2),  # diversity set: N <= 32768
     (dict(kept_feats=(1 << 40) + (1 << 32) + 4096 * 64), 1),  # overlaps vis_feats
     (dict(ratio_mode=2), 1), (dict(ratio_mode=1, score_out=(1 << 40) + (5 << 32)), 1),
     (dict(ratio_mode=1, norm_stats=(1 << 40) + (5 << 32)), 1),
@@ -131,6 +132,18 @@ def test_prellm_rejects_before_launch(bad, code):
     a = _prellm(**bad)
     assert L.trevs_prellm_workspace_size(ctypes.byref(a)) == 0
     assert L.trevs_prellm_prune(ctypes.byref(a), None, 0, None) == code
+
+
+def test_selection_limits():
+    """One selection ranks up to 65,536 tokens (64 per thread); the diversity
+    set's Gram matrix limits it to 32,768."""
+    L = trevs.lib()
+    assert trevs.MAX_SELECT_N == 65536 and trevs.MAX_FPS_N == 32768
+    assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm(N=65536, k_keep=10, n_seg=1))) > 0
+    assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm(N=65537, k_keep=10, n_seg=1))) == 0
+    assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm(N=32768, k_keep=10, n_seg=1, k_div=3))) > 0
+    assert L.trevs_prellm_workspace_size(ctypes.byref(_prellm(N=32769, k_keep=10, n_seg=1, k_div=3))) == 0
+    assert L.trevs_inllm_workspace_size(ctypes.byref(_inllm(K_in=65536, S=65600, T_max=10))) > 0
 
 
 def test_prellm_workspace_errors():
@@ -146,7 +159,7 @@ def test_prellm_workspace_errors():
     (dict(T_max=300), 1), (dict(H_kv=5), 1), (dict(n_keep_heads=0), 1),
     (dict(n_keep_heads=33), 1), (dict(k_keep=193), 1), (dict(scale=0.0), 1), (dict(P=-1), 1),
     (dict(hidden_out=None), 1), (dict(d_head=96), 2), (dict(D=4095), 1), (dict(pos=(1 << 40) + 4), 1),
-    (dict(K_in=40000, S=40100, T_max=10), 2),
+    (dict(K_in=70000, S=70100, T_max=10), 2),
     (dict(k_out=(1 << 40) + (1 << 32) + 1024), 1),  # overlaps k
     (dict(softmax=2), 1), (dict(softmax=-1), 1),
     (dict(softmax=1, lse_rest=(1 << 40) + (11 << 32)), 1),  # lse_rest is for the visual domain
@@ -162,7 +175,7 @@ def test_topk_rejects_before_launch():
     L = trevs.lib()
     assert L.trevs_topk_select(1 << 40, 1, 10, 11, (1 << 40) + (1 << 32), None, 0, None) == 1
     assert L.trevs_topk_select(None, 1, 10, 1, (1 << 40) + (1 << 32), None, 0, None) == 1
-    assert L.trevs_topk_select(1 << 40, 1, 40000, 1, (1 << 40) + (1 << 32), None, 0, None) == 2
+    assert L.trevs_topk_select(1 << 40, 1, 70000, 1, (1 << 40) + (1 << 32), None, 0, None) == 2
     assert L.trevs_topk_select(1 << 40, 1, 10, 5, (1 << 40) + 8, None, 0, None) == 1  # overlap
 
 
@@ -220,7 +233,7 @@ def test_spearman_rejects_before_launch():
     assert L.trevs_topk_spearman(None, st, 2, 100, 30, rho, idx, ws, need, None) == 1
     assert L.trevs_topk_spearman(sv, st, 2, 100, 30, rho + 4, idx, ws, need, None) == 1
     assert L.trevs_topk_spearman(sv, st, 2, 100, 30, sv + 8, idx, ws, need, None) == 1
-    assert L.trevs_topk_spearman(sv, st, 2, 40000, 30, rho, idx, ws, need, None) == 2
+    assert L.trevs_topk_spearman(sv, st, 2, 70000, 30, rho, idx, ws, need, None) == 2
     assert L.trevs_topk_spearman(sv, st, 2, 100, 30, rho, idx, ws, need - 1, None) == 3
     assert L.trevs_topk_spearman(sv, st, 2, 100, 30, rho, idx, None, 0, None) == 3
 

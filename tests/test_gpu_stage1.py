@@ -100,14 +100,16 @@ def test_stage1_keep_extremes(k):
         assert (g["kept_idx"] == np.arange(w.N)).all()
 
 
-@pytest.mark.parametrize("k", [1, 12345, 32768])
-def test_stage1_max_tokens(k):
-    """The largest N one selection supports (32,768 tokens, 32 per selection
-    thread), keeping one token, a ragged count, or every token; text of
-    60-100 rows (the 128-row relevance tile with a ragged tail)."""
-    w = WORKLOADS["llava15-b64-bf16"].with_(B=2, N=32768, K1=k, d=256, M_max=100,
+@pytest.mark.parametrize("N,k", [(32768, 1), (32768, 12345), (32768, 32768),
+                                 (65536, 1), (65536, 23456), (65536, 65536)])
+def test_stage1_max_tokens(N, k):
+    """32,768 tokens (32 per selection thread) and the largest N one
+    selection supports (65,536, 64 per thread), keeping one token, a ragged
+    count, or every token; text of 60-100 rows (the 128-row relevance tile
+    with a ragged tail)."""
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=2, N=N, K1=k, d=256, M_max=100,
                                             text_len=("uniform", 60, 100), n_sal=40, n_qm=40)
-    print(f"[stage1] max tokens, K1={k}", flush=True)
+    print(f"[stage1] max tokens, N={N} K1={k}", flush=True)
     inp = stage1_inputs(w)
     g = run_gpu(inp, w)
     check(inp, w, g, run_oracle(inp, w))
@@ -247,6 +249,9 @@ BUDGET_CASES = {
     "rho0-f32": (WORKLOADS["llava15-b1-f32"], 0.0),
     "rho1-f32": (WORKLOADS["llava15-b1-f32"], 1.0),
     "qwen25vl-b1-bf16-rho0.5": (WORKLOADS["qwen25vl-b4-bf16"].with_(B=1), 0.5),
+    # 64 elements per selection thread (uint64 keep masks)
+    "max-tokens-bf16-rho0.4": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=1, N=65536, K1=20000, d=256, M_max=64, n_sal=40, n_qm=40), 0.4),
 }
 
 

@@ -181,14 +181,16 @@ def test_stage2_keep_extremes(n_keep, k_keep):
         assert (g["head_sel"] == np.arange(w.H_q)).all()
 
 
-@pytest.mark.parametrize("k_keep", [1, 5000, 32768])
-def test_stage2_max_visual_rows(k_keep):
-    """The largest visual block one selection supports (32,768 rows, 32
-    per selection thread), keeping one row, a ragged count, or every row."""
-    w = WORKLOADS["llava15-b64-bf16"].with_(B=1, N=32768, K1=32768, K2=k_keep, M_max=8,
+@pytest.mark.parametrize("K1,k_keep", [(32768, 1), (32768, 5000), (32768, 32768),
+                                       (65536, 1), (65536, 40000), (65536, 65536)])
+def test_stage2_max_visual_rows(K1, k_keep):
+    """32,768 visual rows (32 per selection thread) and the largest block one
+    selection supports (65,536, 64 per thread), keeping one row, a ragged
+    count, or every row."""
+    w = WORKLOADS["llava15-b64-bf16"].with_(B=1, N=K1, K1=K1, K2=k_keep, M_max=8,
                                             text_len=("fixed",), H_q=4, H_kv=2, d_h=64, D=64,
                                             n_keep=2, grid=0)
-    print(f"[stage2] max visual rows, K2={k_keep}", flush=True)
+    print(f"[stage2] max visual rows, K1={K1} K2={k_keep}", flush=True)
     inp = stage2_inputs(w)
     g = run_gpu(inp, w)
     check(inp, w, g)

@@ -19,7 +19,8 @@ def check(scores, k):
 
 @pytest.mark.parametrize("N,K", [(1, 1), (5, 3), (576, 192), (577, 64), (2880, 640),
                                  (4096, 1024), (16384, 4096), (32768, 1), (32768, 32768),
-                                 (1000, 999)])
+                                 (1000, 999), (50000, 12345), (65536, 1), (65536, 40000),
+                                 (65536, 65536)])
 def test_topk_random_with_quantised_ties(N, K):
     print(f"[topk] N={N} K={K}", flush=True)
     rng = np.random.default_rng(N * 7 + K)
@@ -50,7 +51,7 @@ def test_topk_crowded_first_digit_bin():
     candidate list; once with the crowded bin above the minimum, once with
     the minimum itself in it (its ties counted by ballot)."""
     rng = np.random.default_rng(11)
-    for N in (16384, 32768):
+    for N in (16384, 32768, 65536):
         above = rng.random((2, N)).astype(np.float32)
         crowd = rng.random((2, N)) < 0.4
         above[crowd] = np.float32(2.0) + rng.integers(0, 3, size=crowd.sum()).astype(np.float32) * np.float32(2.0 ** -22)
@@ -79,5 +80,5 @@ def test_topk_rejects_bad_arguments():
     with pytest.raises(trevs.TrevsError):
         trevs.topk_select(s, 11)
     with pytest.raises(trevs.TrevsError) as e:
-        trevs.topk_select(torch.zeros((1, 40000), device="cuda"), 5)
+        trevs.topk_select(torch.zeros((1, 70000), device="cuda"), 5)
     assert e.value.status == 2
