@@ -491,7 +491,7 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
     const uint32_t i2 = lane < kSelWaves ? (uint32_t)wi[buf][lane] : 0xffffffffu;
     const float bv = wave_max(v2);
     int w = (int)wave_min_u32(v2 == bv ? i2 : 0xffffffffu);
-    w = min(max(w, 0), N - 1);  // K_r + K_d <= N leaves a candidate at every step
+    w = __builtin_amdgcn_readfirstlane(min(max(w, 0), N - 1));  // K_r + K_d <= N leaves a candidate
     if (tid == 0 && a.div_idx) a.div_idx[(size_t)b * a.K_d + t] = w;
     const int we = w / kSelThreads;
     const bool mine = (w & (kSelThreads - 1)) == tid;
@@ -499,17 +499,27 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
 #pragma unroll
     for (int e = 0; e < E; ++e)
       if (mine && e == we) dist[e] = -INFINITY;
-    const float* row = gb + (size_t)w * N;
+    // the winner's row of G through a buffer resource: a uniform base and a
+    // 32-bit offset per element (no 64-bit address per element), and the
+    // elements past N read 0 (their distance is -inf already)
+    const __amdgpu_buffer_rsrc_t row = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(gb + (size_t)w * N), 0, N * 4, kBufferRsrcWord3);
     const float izw = a.inv_norm[(size_t)b * N + w];
-    // all of the row's loads go out before any is used (one round trip)
-    float gi[E];
+    // the row's loads go out before any is used, up to 16 at a time (one
+    // round trip for N <= 16,384; 32 held values would spill)
+    constexpr int CH = E < 16 ? E : 16;
 #pragma unroll
-    for (int e = 0; e < E; ++e) gi[e] = row[min(e * kSelThreads + tid, N - 1)];
-    __builtin_amdgcn_sched_barrier(0);
+    for (int c0 = 0; c0 < E; c0 += CH) {
+      float gi[CH];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const float d = 1.f - gi[e] * iz[e] * izw;
-      dist[e] = d < dist[e] ? d : dist[e];
+      for (int u = 0; u < CH; ++u)
+        gi[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(row, ((c0 + u) * kSelThreads + tid) * 4, 0, 0));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < CH; ++u) {
+        const float d = 1.f - gi[u] * iz[c0 + u] * izw;
+        dist[c0 + u] = d < dist[c0 + u] ? d : dist[c0 + u];
+      }
     }
   }
   block_write_mask<E>(sel, K_r + a.K_d, a.kept_idx + (size_t)b * (K_r + a.K_d), sh);

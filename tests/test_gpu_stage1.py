@@ -311,6 +311,9 @@ FPS_CASES = {
         B=2, N=4096, d=1024, K1=512, n_sal=8, n_qm=10), 128),
     "gram256-tail64-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
         B=2, N=2310, d=544, K1=300, n_sal=8, n_qm=10), 100),
+    # 32 elements per picks thread (N > 16,384): the row is read 16 values a time
+    "e32-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=1, N=20000, d=256, K1=40, n_sal=8, n_qm=10), 20),
 }
 
 
