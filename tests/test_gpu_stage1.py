@@ -290,6 +290,45 @@ def test_stage1_budget_split(name):
         assert agree > 0.95, (b, agree)
 
 
+def test_stage1_budget_split_with_diversity_set():
+    """The budget split (Sec. 3 reading) as the pivot rule of context
+    preservation (Sec. 4.1): the K_r pivots are exactly the oracle's budget
+    split of the kernel's own s^v and s^t, and every pick is the farthest
+    unselected token from the GPU's own selected set (within the near-tie
+    band of the float64 distances)."""
+    w, rho, k_div = WORKLOADS["llava15-b64-bf16"].with_(B=2), 0.3, 48
+    print(f"[stage1-budget-fps] B={w.B} N={w.N} K1={w.K1} K_d={k_div} rho={rho}", flush=True)
+    inp = stage1_inputs(w)
+    cls = dev_tensor(inp["cls_logits"], w.dtype)
+    Z = dev_tensor(inp["vis_feats"], w.dtype)
+    T = dev_tensor(inp["text_emb"], w.dtype)
+    tl = torch.from_numpy(inp["text_len"]).cuda()
+    call = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, k_div=k_div, n_seg=w.n_seg, textual_ratio=rho,
+                        want_scores=True, ratio_mode="budget")
+    call()
+    torch.cuda.synchronize()
+    kept = call.kept_idx.cpu().numpy()
+    picks = call.div_idx.cpu().numpy()
+    feats = host_bits(call.kept_feats)
+    sal, rel = call.sal.cpu().numpy(), call.rel.cpu().numpy()
+    rho32 = float(np.float32(rho))
+    o = oracle.prellm(inp["cls_logits"], inp["vis_feats"], inp["text_emb"], inp["text_len"],
+                      w.dtype, n_seg=w.n_seg, k_keep=w.K1, k_div=k_div, rho=rho32, ratio_mode="budget")
+    assert_scores_close(sal, o["sal"], "s^v")
+    assert_scores_close(rel, o["rel"], "s^t")
+    K_r = w.K1 - k_div
+    for b in range(w.B):
+        pivots = np.setdiff1d(kept[b], picks[b])
+        want_piv = oracle.budget_split_topk(sal[b].astype(np.float64), rel[b].astype(np.float64), K_r, rho32)
+        assert np.array_equal(pivots, np.sort(want_piv)), b
+        assert np.array_equal(kept[b], np.sort(np.concatenate([pivots, picks[b]]))), b
+        assert np.array_equal(feats[b], inp["vis_feats"][b][kept[b]]), b
+        Z64 = oracle.to_f64(inp["vis_feats"][b], w.dtype)
+        want = oracle.farthest_point_sampling(Z64, pivots, k_div)
+        same = check_fps_picks(Z64, pivots, picks[b], want)
+        print(f"[stage1-budget-fps] b={b}: {same}/{k_div} picks equal the oracle's sequence", flush=True)
+
+
 # ------------------------------------------------------------- diversity set
 FPS_CASES = {
     "llava15-b2-bf16": (WORKLOADS["llava15-b64-bf16"].with_(B=2), 48),
