@@ -23,7 +23,7 @@ namespace trevs {
 // (rows XOR-swizzled by 16-byte chunk), and the waves multiply on the matrix
 // cores, each a 64x64 block.  Bytes past a row's end (a partial last slab)
 // load as zero.  The tile is written in place and, off the diagonal, also
-// transposed through LDS (rows padded to 129 floats) with coalesced stores.
+// transposed; both go through LDS and out as 16-byte runs of whole rows.
 // Diagonal tiles also write 1/max(||z_i||, 1e-12) from G_ii.  G is written
 // with nontemporal stores: the picks read it back long after it has left the
 // caches, and cached stores would evict operand slabs the other resident
@@ -52,9 +52,7 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   constexpr int T = kGramTile;
   constexpr int SLAB = T * 128;                  // bytes of one operand slab
   constexpr int VPT = SLAB / 16 / kGramThreads;  // vectors per thread per operand
-  constexpr int TP = T + 1;                      // padded row of the staged tile (floats)
-  constexpr int LDS = 4 * SLAB > T * TP * 4 ? 4 * SLAB : T * TP * 4;
-  // two operand-slab buffers during the product, then the finished tile
+  constexpr int LDS = 4 * SLAB;                  // two stages of both operand slabs, then the output passes
   __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS];
   uint8_t* l0 = lds;
   uint8_t* l1 = lds + 2 * SLAB;
@@ -157,18 +155,6 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   }
   // output: register r of block (m, n) is row wj*64 + m*32 + mfma_row(r),
   // column wi*64 + n*32 + col of the tile
-  float* gb = a.G + (size_t)b * N * N;
-#pragma unroll
-  for (int m = 0; m < 2; ++m)
-#pragma unroll
-    for (int n = 0; n < 2; ++n) {
-      const int i = ti * T + wi * 64 + n * 32 + col;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = tj * T + wj * 64 + m * 32 + mfma_row(r, half);
-        if (i < N && j < N) __builtin_nontemporal_store(acc[m][n][r], &gb[(size_t)j * N + i]);
-      }
-    }
   if (tj == ti) {  // the diagonal tile holds ||z_i||^2
 #pragma unroll
     for (int m = 0; m < 2; ++m)
@@ -181,24 +167,64 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
           if (jl == il && i < N)
             a.inv_norm[(size_t)b * N + i] = 1.f / fmaxf(sqrtf(fmaxf(acc[m][n][r], 0.f)), 1e-12f);
         }
-    return;
   }
-  // the mirrored tile G[i, j] through LDS: stage tile[jl][il], then write
-  // rows il with consecutive jl per lane
-  __syncthreads();  // every wave is done with the operand slabs
-  float* tile = reinterpret_cast<float*>(lds);
+  // The tile leaves through LDS, 32 rows j at a time, as 16-byte runs of
+  // whole rows: tA (rows j, stride TA: 16-byte aligned rows, the half-waves'
+  // writes on disjoint banks) for G[j, i]; off the diagonal tB (rows i, odd
+  // stride TB) for the mirrored G[i, j].  Whole tiles of a matrix whose rows
+  // are a multiple of 16 bytes store without bounds checks.
+  constexpr int TA = T + 8, TB = 33, PR = 32;
+  static_assert((PR * TA + T * TB) * 4 <= LDS, "output staging fits the LDS");
+  float* tA = reinterpret_cast<float*>(lds);
+  float* tB = tA + PR * TA;
+  float* gb = a.G + (size_t)b * N * N;
+  const bool mirror = tj != ti;
+  const bool fast = (ti + 1) * T <= N && (N & 3) == 0;  // tj <= ti
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int p = 0; p < T / PR; ++p) {  // unrolled: the accumulator block m is a constant
+    __syncthreads();  // the operand slabs, or the previous pass, are no longer read
+    if (wj == p / 2) {
+      const int m = p % 2;
 #pragma unroll
-    for (int n = 0; n < 2; ++n)
+      for (int n = 0; n < 2; ++n)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        tile[(wj * 64 + m * 32 + mfma_row(r, half)) * TP + wi * 64 + n * 32 + col] = acc[m][n][r];
-  __syncthreads();
-  for (int e = tid; e < T * T; e += kGramThreads) {
-    const int il = e / T, jl = e - il * T;
-    const int i = ti * T + il, j = tj * T + jl;
-    if (i < N && j < N) __builtin_nontemporal_store(tile[jl * TP + il], &gb[(size_t)i * N + j]);
+        for (int r = 0; r < 16; ++r) {
+          const int jl = mfma_row(r, half), il = wi * 64 + n * 32 + col;
+          tA[jl * TA + il] = acc[m][n][r];
+          if (mirror) tB[il * TB + jl] = acc[m][n][r];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < PR * T / 4 / kGramThreads; ++k) {  // G[j, i]: PR rows of T / 4 runs
+      const int e = tid + k * kGramThreads, row = e / (T / 4), q = e % (T / 4);
+      const int j = tj * T + PR * p + row, i = ti * T + 4 * q;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(&tA[row * TA + 4 * q]);
+      if (fast) {
+        stg16_stream(&gb[(size_t)j * N + i], v);
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (j < N && i + u < N) __builtin_nontemporal_store(__uint_as_float(v[u]), &gb[(size_t)j * N + i + u]);
+      }
+    }
+    if (mirror) {  // G[i, j]: T rows of PR / 4 runs
+#pragma unroll
+      for (int k = 0; k < PR * T / 4 / kGramThreads; ++k) {
+        const int e = tid + k * kGramThreads, il = e / (PR / 4), q = e % (PR / 4);
+        const int i = ti * T + il, j = tj * T + PR * p + 4 * q;
+        const float* src = &tB[il * TB + 4 * q];
+        const u32x4 v = {__float_as_uint(src[0]), __float_as_uint(src[1]), __float_as_uint(src[2]),
+                         __float_as_uint(src[3])};
+        if (fast) {
+          stg16_stream(&gb[(size_t)i * N + j], v);
+        } else {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (i < N && j + u < N) __builtin_nontemporal_store(__uint_as_float(v[u]), &gb[(size_t)i * N + j + u]);
+        }
+      }
+    }
   }
 }
 
@@ -210,8 +236,8 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
 // workgroup per CU).  The fragments are read from LDS one 32-byte k-step at
 // a time to keep the accumulators, the staging ring and the fragments within
 // 256 registers.  Same swizzle, zero fill of a partial slab, super-block
-// order and outputs as gram_kernel; the mirrored tile goes through LDS in
-// four passes of 64 rows.
+// order and outputs as gram_kernel; both output tiles leave through LDS as
+// 16-byte runs of whole rows.
 // ---------------------------------------------------------------------------
 constexpr int kGram256Threads = 512;
 constexpr int kGram256MinN = 2048;
@@ -221,8 +247,6 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
   constexpr int T = 256;
   constexpr int SLAB = T * 128;                     // bytes of one operand slab
   constexpr int VPT = SLAB / 16 / kGram256Threads;  // 4 vectors per thread per operand
-  constexpr int TP = T + 1;                         // padded row of a staged 64-row pass (floats)
-  static_assert(64 * TP * 4 <= 4 * SLAB, "mirror staging fits the operand buffers");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * SLAB];
   uint8_t* l0 = lds;
   uint8_t* l1 = lds + 2 * SLAB;
@@ -324,18 +348,6 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
   }
   // register r of block (m, n) is row wj*128 + m*32 + mfma_row(r), column
   // wi*64 + n*32 + col of the tile
-  float* gbm = a.G + (size_t)b * N * N;
-#pragma unroll
-  for (int m = 0; m < 4; ++m)
-#pragma unroll
-    for (int n = 0; n < 2; ++n) {
-      const int i = ti * T + wi * 64 + n * 32 + col;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = tj * T + wj * 128 + m * 32 + mfma_row(r, half);
-        if (i < N && j < N) __builtin_nontemporal_store(acc[m][n][r], &gbm[(size_t)j * N + i]);
-      }
-    }
   if (tj == ti) {  // the diagonal tile holds ||z_i||^2
 #pragma unroll
     for (int m = 0; m < 4; ++m)
@@ -348,31 +360,67 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
           if (jl == il && i < N)
             a.inv_norm[(size_t)b * N + i] = 1.f / fmaxf(sqrtf(fmaxf(acc[m][n][r], 0.f)), 1e-12f);
         }
-    return;
   }
-  // the mirrored tile G[i, j], 64 tile rows jl at a time: the two waves'
-  // 32-row blocks of the pass stage tile[jl - 64p][il], then every thread
-  // writes rows il with consecutive jl per lane
-  float* tile = reinterpret_cast<float*>(lds);
+  // The tile leaves through LDS, 32 rows j at a time, and is stored as
+  // 16-byte runs of whole rows (each lane storing 4 bytes, or 16-byte runs
+  // of a few bytes per row, writes G at a fraction of the rate): tA holds
+  // the pass as rows j (stride TA: 16-byte aligned rows, the two half-waves'
+  // writes on disjoint banks) for G[j, i]; off the diagonal tB holds it as
+  // rows i (odd stride TB: the column writes spread over the banks) for the
+  // mirrored G[i, j].  Whole tiles of a matrix whose rows are a multiple of
+  // 16 bytes store without bounds checks.
+  constexpr int TA = T + 8, TB = 33, PR = 32;
+  static_assert((PR * TA + T * TB) * 4 <= 4 * SLAB, "output staging fits the operand buffers");
+  float* tA = reinterpret_cast<float*>(lds);
+  float* tB = tA + PR * TA;
+  float* gbm = a.G + (size_t)b * N * N;
+  const bool mirror = tj != ti;
+  const bool fast = (ti + 1) * T <= N && (N & 3) == 0;  // tj <= ti
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
+  for (int p = 0; p < T / PR; ++p) {  // unrolled: the accumulator block m is a constant
     __syncthreads();  // the operand slabs, or the previous pass, are no longer read
-    if (wj == p / 2) {
+    if (wj == p / 4) {
+      const int m = p % 4;
 #pragma unroll
-      for (int mm = 0; mm < 2; ++mm) {
-        const int m = 2 * (p % 2) + mm;
+      for (int n = 0; n < 2; ++n)
 #pragma unroll
-        for (int n = 0; n < 2; ++n)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            tile[(mm * 32 + mfma_row(r, half)) * TP + wi * 64 + n * 32 + col] = acc[m][n][r];
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int jl = mfma_row(r, half), il = wi * 64 + n * 32 + col;
+          tA[jl * TA + il] = acc[m][n][r];
+          if (mirror) tB[il * TB + jl] = acc[m][n][r];
+        }
     }
     __syncthreads();
-    for (int e = tid; e < T * 64; e += kGram256Threads) {
-      const int il = e >> 6, jl = e & 63;
-      const int i = ti * T + il, j = tj * T + 64 * p + jl;
-      if (i < N && j < N) __builtin_nontemporal_store(tile[jl * TP + il], &gbm[(size_t)i * N + j]);
+    // G[j, i]: PR rows of T / 4 runs
+#pragma unroll
+    for (int k = 0; k < PR * T / 4 / kGram256Threads; ++k) {
+      const int e = tid + k * kGram256Threads, row = e / (T / 4), q = e % (T / 4);
+      const int j = tj * T + PR * p + row, i = ti * T + 4 * q;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(&tA[row * TA + 4 * q]);
+      if (fast) {
+        stg16_stream(&gbm[(size_t)j * N + i], v);
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (j < N && i + u < N) __builtin_nontemporal_store(__uint_as_float(v[u]), &gbm[(size_t)j * N + i + u]);
+      }
+    }
+    if (mirror) {  // G[i, j]: T rows of PR / 4 runs
+#pragma unroll
+      for (int k = 0; k < PR * T / 4 / kGram256Threads; ++k) {
+        const int e = tid + k * kGram256Threads, il = e / (PR / 4), q = e % (PR / 4);
+        const int i = ti * T + il, j = tj * T + PR * p + 4 * q;
+        const float* src = &tB[il * TB + 4 * q];
+        const u32x4 v = {__float_as_uint(src[0]), __float_as_uint(src[1]), __float_as_uint(src[2]),
+                         __float_as_uint(src[3])};
+        if (fast) {
+          stg16_stream(&gbm[(size_t)i * N + j], v);
+        } else {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (i < N && j + u < N) __builtin_nontemporal_store(__uint_as_float(v[u]), &gbm[(size_t)i * N + j + u]);
+        }
+      }
     }
   }
 }
