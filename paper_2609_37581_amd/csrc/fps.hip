@@ -471,10 +471,11 @@ __global__ __launch_bounds__(kFpsInitThreads) void fps_init_kernel(FpsArgs a) {
 // ---------------------------------------------------------------------------
 // The picks: one workgroup per sample walks the K_d sequential steps with
 // the distances of its tokens in registers (element e*1024 + t of thread t,
-// as in the selection kernels).  Each step reduces (distance desc, index
-// asc) over the unselected tokens, marks the winner, and lowers every
-// distance with the winner's row of G.  The selected set (pivots and picks)
-// is then written in ascending order.
+// as in the selection kernels), formed from the initial pass's per-split
+// maxima.  Each step reduces (distance desc, index asc) over the unselected
+// tokens, marks the winner, and lowers every distance with the winner's row
+// of G.  The selected set (pivots and picks) is then written in ascending
+// order.
 // ---------------------------------------------------------------------------
 template <int E>
 __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
