@@ -229,27 +229,41 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Gram matrix at 256x256 tiles (N >= kGram256MinN): a workgroup of 8 waves,
-// each wave a 128x64 block (4x2 MFMA tiles), so every byte streamed from
-// L2 feeds twice the multiplies of the 128-tile form; the pass is bound by
-// the bytes in flight per CU, which stay the same (two 64 KB stages, one
-// workgroup per CU).  The fragments are read from LDS one 32-byte k-step at
-// a time to keep the accumulators, the staging ring and the fragments within
-// 256 registers.  Same swizzle, zero fill of a partial slab, super-block
-// order and outputs as gram_kernel; both output tiles leave through LDS as
-// 16-byte runs of whole rows.
+// Gram matrix at 256x256 tiles, bf16 (N >= kGram256MinN, N + 256 rows of Z
+// under 2 GB; fp32 inputs use gram_kernel; rows are a multiple of 16 bytes): a
+// workgroup of 4 waves, one per SIMD, each a 128x128 block (4x4 MFMA tiles,
+// 256 accumulation registers), so that each fragment byte read from LDS
+// feeds 4 multiplies.  The feature dimension streams in 128-byte stages
+// (four k-steps), loaded 8 lanes to a row (whole 128-byte lines: 4 lanes to
+// a row, 64 bytes, cost about a tenth of the Gram's time) into a ring of two
+// register stages, then into two LDS buffers.  Stage P runs in two halves:
+// the first multiplies k-steps 0-1 while it stores stage P + 1 into the
+// other buffer (free since the last barrier) and loads stage P + 3 into the
+// register stage it frees; after a barrier, the second multiplies k-steps
+// 2-3 while it reads stage P + 1's first fragments.  Every k-step's
+// fragments are read during the previous k-step's multiplies, so each half
+// starts on fragments already in registers.  The loads are buffer loads:
+// chunks past a row's end, rows past N and stages past the last read zeros,
+// which the multiplies add exactly, so the steps need no branches.  Rows are
+// XOR-swizzled in 16-byte chunks (chunk ^ ((row >> 1) & 7)): the stores (2
+// rows x 128 bytes per 16 lanes) and the fragment reads (16 rows at one
+// chunk) hit all 64 banks.  Same super-block order and outputs as
+// gram_kernel; both output tiles leave through LDS as 16-byte runs of whole
+// rows.
 // ---------------------------------------------------------------------------
-constexpr int kGram256Threads = 512;
+constexpr int kGram256Threads = 256;
 constexpr int kGram256MinN = 2048;
 
-template <class In>
-__global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a) {
+__global__ __launch_bounds__(kGram256Threads, 1) void gram256_kernel(GramArgs a) {
   constexpr int T = 256;
-  constexpr int SLAB = T * 128;                     // bytes of one operand slab
-  constexpr int VPT = SLAB / 16 / kGram256Threads;  // 4 vectors per thread per operand
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * SLAB];
-  uint8_t* l0 = lds;
-  uint8_t* l1 = lds + 2 * SLAB;
+  constexpr int SLAB = T * 128;                     // bytes of one operand's 128-byte stage
+  constexpr int VPT = SLAB / 16 / kGram256Threads;  // 8 vectors per thread per operand
+  constexpr int RSTEP = kGram256Threads / 8;        // rows per load pass (8 lanes a row)
+  constexpr int TA = T + 8, TB = 33, PR = 32;       // output staging (see below)
+  constexpr int LDS_OPS = 4 * SLAB;
+  constexpr int LDS_OUT = (PR * TA + T * TB) * 4;
+  constexpr int LDS = LDS_OPS > LDS_OUT ? LDS_OPS : LDS_OUT;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int nT = a.n_tiles;
@@ -266,96 +280,138 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
   const int tj = sj * gs + loc / gs, ti = (sj + rs) * gs + loc % gs;
   if (tj > ti || ti >= nT) return;  // the whole workgroup: no barrier has run
   const int N = a.N, rb = a.row_bytes;
-  const int n_slabs = (rb + 127) / 128;
-  const int tail = rb & 127;  // bytes of a partial last slab, 0 if none
-  const uint8_t* zb = reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb;
+  const int n_stages = (rb + 127) / 128;
+  // rows past N read zeros (their offsets pass N * rb), and so do the chunks
+  // of a stage that is past the row's end (offset + 2^31): with
+  // (N + 256) * rb < 2^31 no offset wraps.  Rows and columns past N are never
+  // stored.
+  const __amdgpu_buffer_rsrc_t zs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(reinterpret_cast<const uint8_t*>(a.Z) + (size_t)b * N * rb), 0, N * rb,
+      kBufferRsrcWord3);
   const int cr = tid >> 3, cc = tid & 7;
-  const uint8_t* src[2 * VPT];  // row starts (rows past N re-read row N - 1)
-#pragma unroll
-  for (int k = 0; k < VPT; ++k) {
-    const int r = cr + (kGram256Threads / 8) * k;
-    src[k] = zb + (size_t)min(tj * T + r, N - 1) * rb;
-    src[VPT + k] = zb + (size_t)min(ti * T + r, N - 1) * rb;
-  }
-  const int sdst = cr * 128 + gram_swizzle(cr, cc) * 16;  // rows 64 apart share the swizzle
+  // the thread loads chunk cc of rows cr + RSTEP * k of both operands
+  const uint32_t rowA = (uint32_t)(tj * T + cr) * rb + cc * 16;
+  const uint32_t rowB = (uint32_t)(ti * T + cr) * rb + cc * 16;
+  const uint32_t kstride = (uint32_t)RSTEP * rb;
+  // LDS: operand A of buffers 0 and 1, then operand B of buffers 0 and 1
+  // (every fragment address is one register per k-step and operand plus an
+  // immediate offset)
+  const int sdst = cr * 128 + gram_swizzle(cr, cc) * 16;  // rows RSTEP apart share the swizzle
   u32x4 g[2][2 * VPT];
-  auto load = [&](int s, u32x4 (&dst)[2 * VPT]) {
-    const int off = min(s, n_slabs - 1) * 128 + cc * 16;
-    const int o = off < rb ? off : 0;
-#pragma unroll
-    for (int k = 0; k < 2 * VPT; ++k) dst[k] = ldg16(src[k] + o);
-  };
-  auto store = [&](uint8_t* st, const u32x4 (&v)[2 * VPT], int s) {
+  // stage P; a chunk past the row's end (and every chunk past the last
+  // stage) takes an offset outside the buffer and reads zeros
+  auto load = [&](int P, u32x4 (&dst)[2 * VPT]) {
+    const uint32_t so = P * 128 + cc * 16 < rb ? (uint32_t)P * 128u : 0x80000000u;
+    const uint32_t oa = rowA + so, ob = rowB + so;
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
-      *reinterpret_cast<u32x4*>(st + sdst + k * (kGram256Threads / 8) * 128) = v[k];
-      *reinterpret_cast<u32x4*>(st + SLAB + sdst + k * (kGram256Threads / 8) * 128) = v[VPT + k];
-    }
-    if (s == n_slabs - 1 && tail && cc * 16 >= tail) {  // chunks past the row's end hold zeros
-#pragma unroll
-      for (int k = 0; k < VPT; ++k) {
-        *reinterpret_cast<u32x4*>(st + sdst + k * (kGram256Threads / 8) * 128) = zero4();
-        *reinterpret_cast<u32x4*>(st + SLAB + sdst + k * (kGram256Threads / 8) * 128) = zero4();
-      }
+      dst[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(zs, oa + k * kstride, 0, 0));
+      dst[VPT + k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(zs, ob + k * kstride, 0, 0));
     }
   };
-  const int wj = wave >> 2, wi = wave & 3;  // rows wj*128.., columns wi*64.. of the tile
-  f32x16 acc[4][2];
+  auto store = [&](int c, const u32x4 (&v)[2 * VPT]) {
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) {
+      *reinterpret_cast<u32x4*>(lds + c * SLAB + sdst + k * RSTEP * 128) = v[k];
+      *reinterpret_cast<u32x4*>(lds + 2 * SLAB + c * SLAB + sdst + k * RSTEP * 128) = v[VPT + k];
+    }
+  };
+  const int wj = wave >> 1, wi = wave & 1;  // rows wj*128.., columns wi*128.. of the tile
+  f32x16 acc[4][4];
 #pragma unroll
   for (int m = 0; m < 4; ++m)
 #pragma unroll
-    for (int n = 0; n < 2; ++n)
+    for (int n = 0; n < 4; ++n)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
-  auto compute = [&](const uint8_t* st) {
+  // fragments of k-step q of a stage: half h holds logical chunk 2q + h.
+  // Every row a lane reads (wj*128 + m*32 + col) has the swizzle of col.
+  const int sw = (col >> 1) & 7;
+  uint32_t fqa[4], fqb[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {  // k-step q: chunk 4*half + q of each row
-      u32x4 fa[4][1], fb[2][1];
+  for (int q = 0; q < 4; ++q) {
+    fqa[q] = (wj * 128 + col) * 128 + ((2 * q + half) ^ sw) * 16;
+    fqb[q] = 2 * SLAB + (wi * 128 + col) * 128 + ((2 * q + half) ^ sw) * 16;
+  }
+  auto frag = [&](int c, int q, u32x4 (&fa)[4][1], u32x4 (&fb)[4][1]) {
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const int row = wj * 128 + m * 32 + col;
-        fa[m][0] = *reinterpret_cast<const u32x4*>(st + row * 128 + gram_swizzle(row, 4 * half + q) * 16);
-      }
+    for (int m = 0; m < 4; ++m) fa[m][0] = *reinterpret_cast<const u32x4*>(lds + fqa[q] + c * SLAB + m * 32 * 128);
 #pragma unroll
-      for (int n = 0; n < 2; ++n) {
-        const int row = wi * 64 + n * 32 + col;
-        fb[n][0] = *reinterpret_cast<const u32x4*>(st + SLAB + row * 128 + gram_swizzle(row, 4 * half + q) * 16);
-      }
+    for (int n = 0; n < 4; ++n) fb[n][0] = *reinterpret_cast<const u32x4*>(lds + fqb[q] + c * SLAB + n * 32 * 128);
+  };
+  auto mfma16 = [&](const u32x4 (&fa)[4][1], const u32x4 (&fb)[4][1]) {
 #pragma unroll
-      for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int n = 0; n < 2; ++n) acc[m][n] = mfma_frag(fa[m], fb[n], acc[m][n], In{});
+      for (int n = 0; n < 4; ++n) acc[m][n] = mfma_frag(fa[m], fb[n], acc[m][n], BF16{});
+  };
+  // an MFMA group of `n` multiplies, each followed by `r` LDS reads, `w` LDS
+  // writes and `l` global loads (the compiler's scheduler fills the groups
+  // in this order)
+  auto interleave = [](auto n, auto r, auto w, auto l) {
+#pragma unroll
+    for (int u = 0; u < decltype(n)::value; ++u) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (decltype(r)::value) __builtin_amdgcn_sched_group_barrier(0x100, decltype(r)::value, 0);
+      if (decltype(w)::value) __builtin_amdgcn_sched_group_barrier(0x200, decltype(w)::value, 0);
+      if (decltype(l)::value) __builtin_amdgcn_sched_group_barrier(0x020, decltype(l)::value, 0);
     }
   };
-  // stage 0's loads go out first: loads complete in order, so the first
-  // store then waits only for them, not for stage 1's as well
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I8 = std::integral_constant<int, 8>;
+  // stage P sits in register stage P % 2 and LDS buffer P % 2
   load(0, g[0]);
   __builtin_amdgcn_sched_barrier(0);
   load(1, g[1]);
-  const int n_iter = (n_slabs + 1) / 2;
+  __builtin_amdgcn_sched_barrier(0);
+  store(0, g[0]);
+  load(2, g[0]);
+  __syncthreads();
+  u32x4 fa0[4][1], fb0[4][1], fa1[4][1], fb1[4][1];
+  frag(0, 0, fa0, fb0);
+  const int n_iter = (n_stages + 1) / 2;
   for (int it = 0; it < n_iter; ++it) {
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const int s = 2 * it + c;
-      uint8_t* st = c ? l1 : l0;
-      // buffer c was last read at step s - 2, before every wave passed the
-      // barrier of step s - 1
-      store(st, g[c], s);
-      load(s + 2, g[c]);
+      const int P = 2 * it + c;
+      // first half: k-steps 0 and 1; stage P + 1 to LDS, stage P + 3 loaded
+      __builtin_amdgcn_sched_barrier(0);
+      frag(c, 1, fa1, fb1);
+      mfma16(fa0, fb0);
+      store(1 - c, g[1 - c]);
+      load(P + 3, g[1 - c]);
+      frag(c, 2, fa0, fb0);
+      mfma16(fa1, fb1);
+      interleave(I8{}, I1{}, I0{}, I0{});
+      interleave(I8{}, I0{}, I2{}, I2{});
+      interleave(I8{}, I0{}, I1{}, I1{});
+      interleave(I8{}, I1{}, I0{}, I0{});
       __syncthreads();
-      if (s < n_slabs) compute(st);
+      // second half: k-steps 2 and 3; stage P + 1's first fragments
+      __builtin_amdgcn_sched_barrier(0);
+      frag(c, 3, fa1, fb1);
+      mfma16(fa0, fb0);
+      frag(1 - c, 0, fa0, fb0);
+      mfma16(fa1, fb1);
+      interleave(I8{}, I1{}, I0{}, I0{});
+      interleave(I8{}, I0{}, I0{}, I0{});
+      interleave(I8{}, I1{}, I0{}, I0{});
+      interleave(I8{}, I0{}, I0{}, I0{});
+      __syncthreads();
     }
   }
   // register r of block (m, n) is row wj*128 + m*32 + mfma_row(r), column
-  // wi*64 + n*32 + col of the tile
+  // wi*128 + n*32 + col of the tile
   if (tj == ti) {  // the diagonal tile holds ||z_i||^2
 #pragma unroll
     for (int m = 0; m < 4; ++m)
 #pragma unroll
-      for (int n = 0; n < 2; ++n)
+      for (int n = 0; n < 4; ++n)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int jl = wj * 128 + m * 32 + mfma_row(r, half), il = wi * 64 + n * 32 + col;
+          const int jl = wj * 128 + m * 32 + mfma_row(r, half), il = wi * 128 + n * 32 + col;
           const int i = ti * T + il;
           if (jl == il && i < N)
             a.inv_norm[(size_t)b * N + i] = 1.f / fmaxf(sqrtf(fmaxf(acc[m][n][r], 0.f)), 1e-12f);
@@ -369,8 +425,6 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
   // rows i (odd stride TB: the column writes spread over the banks) for the
   // mirrored G[i, j].  Whole tiles of a matrix whose rows are a multiple of
   // 16 bytes store without bounds checks.
-  constexpr int TA = T + 8, TB = 33, PR = 32;
-  static_assert((PR * TA + T * TB) * 4 <= 4 * SLAB, "output staging fits the operand buffers");
   float* tA = reinterpret_cast<float*>(lds);
   float* tB = tA + PR * TA;
   float* gbm = a.G + (size_t)b * N * N;
@@ -382,10 +436,10 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
     if (wj == p / 4) {
       const int m = p % 4;
 #pragma unroll
-      for (int n = 0; n < 2; ++n)
+      for (int n = 0; n < 4; ++n)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int jl = mfma_row(r, half), il = wi * 64 + n * 32 + col;
+          const int jl = mfma_row(r, half), il = wi * 128 + n * 32 + col;
           tA[jl * TA + il] = acc[m][n][r];
           if (mirror) tB[il * TB + jl] = acc[m][n][r];
         }
@@ -410,9 +464,9 @@ __global__ __launch_bounds__(kGram256Threads, 2) void gram256_kernel(GramArgs a)
       for (int k = 0; k < PR * T / 4 / kGram256Threads; ++k) {
         const int e = tid + k * kGram256Threads, il = e / (PR / 4), q = e % (PR / 4);
         const int i = ti * T + il, j = tj * T + PR * p + 4 * q;
-        const float* src = &tB[il * TB + 4 * q];
-        const u32x4 v = {__float_as_uint(src[0]), __float_as_uint(src[1]), __float_as_uint(src[2]),
-                         __float_as_uint(src[3])};
+        const float* srcp = &tB[il * TB + 4 * q];
+        const u32x4 v = {__float_as_uint(srcp[0]), __float_as_uint(srcp[1]), __float_as_uint(srcp[2]),
+                         __float_as_uint(srcp[3])};
         if (fast) {
           stg16_stream(&gbm[(size_t)i * N + j], v);
         } else {
@@ -576,14 +630,12 @@ __global__ __launch_bounds__(kSelThreads) void fps_pick_kernel(FpsArgs a) {
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hipStream_t s) {
-  if (g.N >= kGram256MinN) {
+  // rows are a multiple of 16 bytes (checked at the boundary)
+  if (dtype == 1 && g.N >= kGram256MinN && (size_t)(g.N + 256) * g.row_bytes < (1u << 31)) {
     GramArgs g2 = g;
     g2.n_tiles = (g.N + 255) / 256;
     const dim3 ggrid(B * gram_super_pairs(g2.n_tiles) * gram_super(g2.n_tiles) * gram_super(g2.n_tiles));
-    if (dtype == 1)
-      hipLaunchKernelGGL(gram256_kernel<BF16>, ggrid, dim3(kGram256Threads), 0, s, g2);
-    else
-      hipLaunchKernelGGL(gram256_kernel<F32>, ggrid, dim3(kGram256Threads), 0, s, g2);
+    hipLaunchKernelGGL(gram256_kernel, ggrid, dim3(kGram256Threads), 0, s, g2);
   } else {
     const dim3 ggrid(B * gram_super_pairs(g.n_tiles) * gram_super(g.n_tiles) * gram_super(g.n_tiles));
     if (dtype == 1)

@@ -339,13 +339,15 @@ FPS_CASES = {
         text_len=("uniform", 1, 40)), 9),
     "tie-stress-bf16": (WORKLOADS["sweep-llava15-b32-bf16"].with_(B=2, tie_stress=True), 30),
     "one-pivot-bf16": (WORKLOADS["llava15-b64-bf16"].with_(B=1, K1=20), 19),
-    # N >= 2048: the 256-row Gram tiles (ragged N, a partial 128-byte slab,
-    # two super-blocks a side; fp32)
+    # N >= 2048, bf16: the 256-row Gram tiles.  Ragged N with a last stage of
+    # 16 of 128 bytes (its other chunks read zeros), two super-blocks a side
     "gram256-ragged-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
         B=2, N=2500, d=520, K1=300, n_sal=8, n_qm=10), 100),
-    "gram256-f32": (WORKLOADS["llava15-b1-f32"].with_(N=2100, d=256, K1=200), 60),
-    # whole 256-row tiles (N = 4096, two super-blocks a side), and a last
-    # slab of 64 of 128 bytes (zeroed in LDS) with N not a multiple of 4
+    # fp32 at N >= 2048 stays on the 128-row tiles (ragged N)
+    "gram128-f32": (WORKLOADS["llava15-b1-f32"].with_(N=2100, d=256, K1=200), 60),
+    # whole 256-row tiles (N = 4096, two super-blocks a side, an even number
+    # of stages), and an odd number of stages with a last stage of 64 of 128
+    # bytes and N not a multiple of 4
     "gram256-whole-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
         B=2, N=4096, d=1024, K1=512, n_sal=8, n_qm=10), 128),
     "gram256-tail64-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
