@@ -501,6 +501,15 @@ def main():
         extras["row_stats_from_layer"] = {"ms_per_step": rs_ms, "value": w.B * w.N / (rs_ms * 1e-3),
                                           "softmax": "causal"}
         del inl_rs, rs
+        # stage 1 with a diversity set at the 3:1 pivot:diversity split of
+        # Sec. 4.1 (K_d = K1 / 4 farthest-point tokens), then stage 2
+        if args.k_div == 0 and w.N <= trevs.MAX_FPS_N:
+            kd = w.K1 // 4
+            pre_fps = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, n_seg=w.n_seg, textual_ratio=w.rho,
+                                   ratio_mode=args.ratio_mode, k_div=kd)
+            fps_ms = plain_step_ms(pre_fps, inl, stream, 10, 2)
+            extras["diversity_set"] = {"k_div": kd, "ms_per_step": fps_ms, "value": w.B * w.N / (fps_ms * 1e-3)}
+            del pre_fps
 
     nb = algorithmic_bytes(w, s1["text_len"], args.softmax)
     traffic = counter_traffic(w.name)
