@@ -83,7 +83,7 @@ def assert_kept_exact_on_own_scores(gpu_idx, gpu_scores, k, name):
 FPS_TIE = 1e-5  # oracle distances this close are a genuine near-tie
 
 
-def check_fps_picks(Z64, pivots, picks, want):
+def check_fps_picks(Z64, pivots, picks, want=None):
     """Every pick of the GPU sequence is valid against the GPU's own selected
     set so far: it is not yet selected, and its float64 distance to its
     nearest selected token is within FPS_TIE of the largest over the
@@ -91,13 +91,17 @@ def check_fps_picks(Z64, pivots, picks, want):
     forces the unique farthest token, so the sequence equals the oracle's
     `want` until a genuine near-tie, and every later pick is still checked
     against the history the GPU actually took.  Returns the number of picks
-    equal to the oracle's before the first difference."""
+    equal to the oracle's before the first difference (0 without `want`)."""
     zbar = oracle.l2_normalise_rows(Z64)
     N = zbar.shape[0]
+    picks = np.asarray(picks, dtype=np.int64)
     taken = np.zeros(N, dtype=bool)
     taken[np.asarray(pivots, dtype=np.int64)] = True
     dist = (1.0 - zbar @ zbar[np.asarray(pivots, dtype=np.int64)].T).min(axis=1) if len(pivots) \
         else np.zeros(N)
+    # the cosine similarities of every pick to every token in one product
+    # (row t is zbar @ zbar[picks[t]]); indices are checked before each use
+    rows = zbar[np.clip(picks, 0, N - 1)] @ zbar.T
     same = 0
     for t, p in enumerate(picks):
         p = int(p)
@@ -106,8 +110,8 @@ def check_fps_picks(Z64, pivots, picks, want):
             assert p == 0, (t, p)
         best = dist[~taken].max()
         assert dist[p] >= best - FPS_TIE, (t, p, dist[p], best)
-        if same == t and p == int(want[t]):
+        if want is not None and same == t and p == int(want[t]):
             same += 1
         taken[p] = True
-        dist = np.minimum(dist, 1.0 - zbar @ zbar[p])
+        dist = np.minimum(dist, 1.0 - rows[t])
     return same

@@ -214,6 +214,46 @@ def test_stage1_full_size_qwen(qwen_full):
         assert np.isin(inp["matched"][b], g["kept_idx"][b]).mean() > 0.9
 
 
+def test_stage1_diversity_set_full_size_qwen(qwen_full):
+    """The diversity set at the benchmarked shape (B=4, N=16384, d'=3584) with
+    K_d = K1/4 = 1024 farthest-point tokens, the 3:1 split of Sec. 4.1 that
+    the bench times: per sample the pivots are exactly the top-K_r of the
+    kernel's own fused score, the kept list is their ascending union with the
+    picks, the gather is bit-exact, and every one of the 1024 picks is checked
+    against float64 distances to the GPU's own selected set so far (the
+    scores themselves are checked at this shape by the full-size test above).  The oracle's own pick sequence is not
+    computed here: it recomputes every distance to the whole selected set at
+    each pick."""
+    w, inp = qwen_full
+    k_div = w.K1 // 4
+    print(f"[stage1-fps] full-size qwen: K_d={k_div}", flush=True)
+    cls = dev_tensor(inp["cls_logits"], w.dtype)
+    Z = dev_tensor(inp["vis_feats"], w.dtype)
+    T = dev_tensor(inp["text_emb"], w.dtype)
+    tl = torch.from_numpy(inp["text_len"]).cuda()
+    call = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, k_div=k_div, n_seg=w.n_seg,
+                        textual_ratio=w.rho, want_scores=True)
+    call()
+    torch.cuda.synchronize()
+    kept = call.kept_idx.cpu().numpy()
+    picks = call.div_idx.cpu().numpy()
+    feats = host_bits(call.kept_feats)
+    score = call.score.cpu().numpy()
+    del call, cls, Z, T
+    K_r = w.K1 - k_div
+    for b in range(w.B):
+        pivots = np.setdiff1d(kept[b], picks[b])
+        assert pivots.size == K_r and np.unique(picks[b]).size == k_div, b
+        assert np.array_equal(pivots, oracle.topk_ascending(score[b].astype(np.float64), K_r)), b
+        assert np.array_equal(kept[b], np.sort(np.concatenate([pivots, picks[b]]))), b
+        assert np.array_equal(feats[b], inp["vis_feats"][b][kept[b]]), b
+    for b in range(w.B):
+        pivots = np.setdiff1d(kept[b], picks[b])
+        Z64 = oracle.to_f64(inp["vis_feats"][b], w.dtype)
+        check_fps_picks(Z64, pivots, picks[b])
+        print(f"[stage1-fps] full-size qwen b={b}: {k_div} picks validated", flush=True)
+
+
 def test_stage1_run_to_run_bit_identical(qwen_full):
     w, inp = qwen_full
     a = run_gpu(inp, w)
