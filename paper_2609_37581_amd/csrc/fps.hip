@@ -32,17 +32,46 @@ namespace trevs {
 constexpr int kGramTile = 128;
 constexpr int kGramThreads = 256;
 
-// Workgroup order: the tile pairs are walked in super-blocks of gs x gs
-// tiles (gs = min(8, tiles per side)), so that the ~64 workgroups resident on
-// one XCD at a time share 2*gs row blocks of Z and each slab they stream is
-// reused from L2 by gs workgroups (in row-major tile order they shared one
-// row block and streamed 64 distinct ones).  Super-blocks on and above the
-// diagonal are numbered row-major; a slot below the diagonal (or past the
-// last tile) exits at once.
+// Workgroup order: the tiles on and above the diagonal are walked in
+// super-blocks of gs x gs tiles (gs = min(8, tiles per side)), so that the
+// workgroups resident on one XCD at a time share 2*gs row blocks of Z and
+// each slab they stream is reused from L2 by up to gs workgroups (in
+// row-major tile order they shared one row block and streamed 64 distinct
+// ones).  Super-blocks are numbered row-major over the pairs sj <= si, and
+// every workgroup gets a tile: a diagonal super-block holds only its tiles
+// on and above the diagonal (row-major), so the workgroups resident at one
+// time cover compact runs of tiles instead of slots that exit at once.
 __host__ __device__ constexpr int gram_super(int n_tiles) { return n_tiles < 8 ? n_tiles : 8; }
-__host__ __device__ constexpr int gram_super_pairs(int n_tiles) {
-  return ((n_tiles + gram_super(n_tiles) - 1) / gram_super(n_tiles)) *
-         ((n_tiles + gram_super(n_tiles) - 1) / gram_super(n_tiles) + 1) / 2;
+__host__ __device__ constexpr int gram_tiles(int n_tiles) { return n_tiles * (n_tiles + 1) / 2; }
+
+// tile (tj, ti), tj <= ti, of dense index t in [0, gram_tiles(nT))
+__device__ __forceinline__ void gram_tile_of(int t, int nT, int& tj, int& ti) {
+  const int gs = gram_super(nT), nS = (nT + gs - 1) / gs;
+  tj = 0;
+  ti = 0;
+  for (int sj = 0; sj < nS; ++sj) {
+    const int h = min(gs, nT - sj * gs);
+    for (int si = sj; si < nS; ++si) {
+      const int w = min(gs, nT - si * gs);
+      const int cnt = si == sj ? h * (h + 1) / 2 : h * w;
+      if (t < cnt) {
+        if (si == sj) {
+          int r = 0;
+          while (t >= h - r) {
+            t -= h - r;
+            ++r;
+          }
+          tj = sj * gs + r;
+          ti = sj * gs + r + t;
+        } else {
+          tj = sj * gs + t / w;
+          ti = si * gs + t % w;
+        }
+        return;
+      }
+      t -= cnt;
+    }
+  }
 }
 
 __device__ __forceinline__ int gram_swizzle(int r, int c) { return c ^ ((r >> 1) & 7); }
@@ -59,18 +88,11 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int nT = a.n_tiles;
-  const int gs = gram_super(nT), nS = (nT + gs - 1) / gs;
-  const int per_b = gram_super_pairs(nT) * gs * gs;
+  const int per_b = gram_tiles(nT);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int b = lin / per_b;
-  const int rem = lin - b * per_b, sp = rem / (gs * gs), loc = rem - sp * gs * gs;
-  int sj = 0, rs = sp;  // super-block pair (sj <= si), row-major
-  while (rs >= nS - sj) {
-    rs -= nS - sj;
-    ++sj;
-  }
-  const int tj = sj * gs + loc / gs, ti = (sj + rs) * gs + loc % gs;
-  if (tj > ti || ti >= nT) return;  // the whole workgroup: no barrier has run
+  int tj, ti;
+  gram_tile_of(lin - b * per_b, nT, tj, ti);
   const int N = a.N, rb = a.row_bytes;
   const int n_slabs = (rb + 127) / 128;
   const int tail = rb & 127;  // bytes of a partial last slab, 0 if none
@@ -267,18 +289,11 @@ __global__ __launch_bounds__(kGram256Threads, 1) void gram256_kernel(GramArgs a)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int nT = a.n_tiles;
-  const int gs = gram_super(nT), nS = (nT + gs - 1) / gs;
-  const int per_b = gram_super_pairs(nT) * gs * gs;
+  const int per_b = gram_tiles(nT);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int b = lin / per_b;
-  const int rem = lin - b * per_b, sp = rem / (gs * gs), loc = rem - sp * gs * gs;
-  int sj = 0, rs = sp;
-  while (rs >= nS - sj) {
-    rs -= nS - sj;
-    ++sj;
-  }
-  const int tj = sj * gs + loc / gs, ti = (sj + rs) * gs + loc % gs;
-  if (tj > ti || ti >= nT) return;  // the whole workgroup: no barrier has run
+  int tj, ti;
+  gram_tile_of(lin - b * per_b, nT, tj, ti);
   const int N = a.N, rb = a.row_bytes;
   const int n_stages = (rb + 127) / 128;
   // rows past N read zeros (their offsets pass N * rb), and so do the chunks
@@ -633,10 +648,10 @@ hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hip
   if (dtype == 1 && g.N >= kGram256MinN && (size_t)(g.N + 256) * g.row_bytes < (1u << 31)) {
     GramArgs g2 = g;
     g2.n_tiles = (g.N + 255) / 256;
-    const dim3 ggrid(B * gram_super_pairs(g2.n_tiles) * gram_super(g2.n_tiles) * gram_super(g2.n_tiles));
+    const dim3 ggrid(B * gram_tiles(g2.n_tiles));
     hipLaunchKernelGGL(gram256_kernel, ggrid, dim3(kGram256Threads), 0, s, g2);
   } else {
-    const dim3 ggrid(B * gram_super_pairs(g.n_tiles) * gram_super(g.n_tiles) * gram_super(g.n_tiles));
+    const dim3 ggrid(B * gram_tiles(g.n_tiles));
     if (dtype == 1)
       hipLaunchKernelGGL(gram_kernel<BF16>, ggrid, dim3(kGramThreads), 0, s, g);
     else
