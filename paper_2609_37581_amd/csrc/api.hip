@@ -494,6 +494,7 @@ trevs_status trevs_prellm_prune(const trevs_prellm_args* a, void* ws, size_t ws_
   if (a->k_div > 0) {
     GramArgs ga;
     ga.Z = a->vis_feats;
+    ga.B = a->B;
     ga.N = a->N;
     ga.row_bytes = a->d * e;
     ga.n_tiles = (a->N + 127) / 128;

@@ -74,6 +74,33 @@ __device__ __forceinline__ void gram_tile_of(int t, int nT, int& tj, int& ti) {
   }
 }
 
+// Workgroup -> (sample b, dense tile index t).  With many tiles per sample
+// (kGramStripe or more) XCD x takes the x-th eighth of every sample's tiles
+// (a contiguous run in super-block order, for its L2), sample after sample,
+// so that at any time all XCDs stream the same sample's Z, which fits the
+// last-level cache (all samples together need not); workgroups go to the 8
+// XCDs round-robin, and the grid, 8 * B * ceil(tiles / 8), has a few padding
+// workgroups (false).  With few tiles per sample each XCD keeps whole
+// samples instead (a contiguous range of workgroups per XCD), so that a
+// sample's Z is loaded into one L2 only.
+constexpr int kGramStripe = 64;
+__device__ __forceinline__ bool gram_work(int per_b, int B, int& b, int& t) {
+  if (per_b < kGramStripe) {
+    const int lin = xcd_remap(blockIdx.x, gridDim.x);
+    b = lin / per_b;
+    t = lin - b * per_b;
+    return true;
+  }
+  const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
+  const int r0 = (x * per_b) >> 3, L = (((x + 1) * per_b) >> 3) - r0;  // L >= 8
+  b = k / L;
+  t = r0 + (k - b * L);
+  return b < B;
+}
+__host__ __device__ constexpr int gram_grid(int n_tiles, int B) {
+  return gram_tiles(n_tiles) < kGramStripe ? B * gram_tiles(n_tiles) : 8 * B * ((gram_tiles(n_tiles) + 7) / 8);
+}
+
 __device__ __forceinline__ int gram_swizzle(int r, int c) { return c ^ ((r >> 1) & 7); }
 
 template <class In>
@@ -88,11 +115,9 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(GramArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int nT = a.n_tiles;
-  const int per_b = gram_tiles(nT);
-  const int lin = xcd_remap(blockIdx.x, gridDim.x);
-  const int b = lin / per_b;
-  int tj, ti;
-  gram_tile_of(lin - b * per_b, nT, tj, ti);
+  int b, t, tj, ti;
+  if (!gram_work(gram_tiles(nT), a.B, b, t)) return;  // the whole workgroup: no barrier has run
+  gram_tile_of(t, nT, tj, ti);
   const int N = a.N, rb = a.row_bytes;
   const int n_slabs = (rb + 127) / 128;
   const int tail = rb & 127;  // bytes of a partial last slab, 0 if none
@@ -289,11 +314,9 @@ __global__ __launch_bounds__(kGram256Threads, 1) void gram256_kernel(GramArgs a)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int nT = a.n_tiles;
-  const int per_b = gram_tiles(nT);
-  const int lin = xcd_remap(blockIdx.x, gridDim.x);
-  const int b = lin / per_b;
-  int tj, ti;
-  gram_tile_of(lin - b * per_b, nT, tj, ti);
+  int b, t, tj, ti;
+  if (!gram_work(gram_tiles(nT), a.B, b, t)) return;  // the whole workgroup: no barrier has run
+  gram_tile_of(t, nT, tj, ti);
   const int N = a.N, rb = a.row_bytes;
   const int n_stages = (rb + 127) / 128;
   // rows past N read zeros (their offsets pass N * rb), and so do the chunks
@@ -648,10 +671,10 @@ hipError_t launch_fps(const FpsArgs& f, const GramArgs& g, int dtype, int B, hip
   if (dtype == 1 && g.N >= kGram256MinN && (size_t)(g.N + 256) * g.row_bytes < (1u << 31)) {
     GramArgs g2 = g;
     g2.n_tiles = (g.N + 255) / 256;
-    const dim3 ggrid(B * gram_tiles(g2.n_tiles));
+    const dim3 ggrid(gram_grid(g2.n_tiles, B));
     hipLaunchKernelGGL(gram256_kernel, ggrid, dim3(kGram256Threads), 0, s, g2);
   } else {
-    const dim3 ggrid(B * gram_tiles(g.n_tiles));
+    const dim3 ggrid(gram_grid(g.n_tiles, B));
     if (dtype == 1)
       hipLaunchKernelGGL(gram_kernel<BF16>, ggrid, dim3(kGramThreads), 0, s, g);
     else

@@ -117,7 +117,7 @@ struct ScoreArgs {
 // ---------------------------------------------------------------- diversity set
 struct GramArgs {
   const void* Z;             // [B,N,d]
-  int N, row_bytes, n_tiles; // n_tiles = ceil(N / 128)
+  int B, N, row_bytes, n_tiles; // n_tiles = ceil(N / tile rows)
   float* G;                  // [B,N,N] fp32 dot products z_j . z_i
   float* inv_norm;           // [B,N] 1 / max(||z_i||, 1e-12)
 };
