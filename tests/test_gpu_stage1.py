@@ -392,6 +392,16 @@ FPS_CASES = {
         B=2, N=4096, d=1024, K1=512, n_sal=8, n_qm=10), 128),
     "gram256-tail64-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
         B=2, N=2310, d=544, K1=300, n_sal=8, n_qm=10), 100),
+    # the smallest 256-row grid (N = 2048, 8 tiles a side) with a single
+    # 128-byte stage; rows of 16 bytes (d = 8: one valid chunk a stage);
+    # 11 tiles a side (66 tiles a sample, the first size striped over the
+    # XCDs sample by sample) with B = 3, so the grid has padding workgroups
+    "gram256-min-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=1, N=2048, d=64, K1=256, n_sal=8, n_qm=10), 64),
+    "gram256-d8-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=1, N=2100, d=8, K1=100, n_sal=8, n_qm=10), 30),
+    "gram256-stripe-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
+        B=3, N=2700, d=256, K1=300, n_sal=8, n_qm=10), 75),
     # 32 elements per picks thread (N > 16,384): the row is read 16 values a time
     "e32-bf16": (WORKLOADS["llava15-b64-bf16"].with_(
         B=1, N=20000, d=256, K1=40, n_sal=8, n_qm=10), 20),
