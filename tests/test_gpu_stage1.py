@@ -214,6 +214,50 @@ def test_stage1_full_size_qwen(qwen_full):
         assert np.isin(inp["matched"][b], g["kept_idx"][b]).mean() > 0.9
 
 
+def _sweep_case(seed):
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 5))
+    N = int(rng.integers(2048, 6001))
+    d = 8 * int(rng.integers(1, 97))
+    K1 = int(rng.integers(64, N // 4 + 1))
+    k_div = int(rng.integers(1, K1 // 2 + 1))
+    return WORKLOADS["llava15-b64-bf16"].with_(B=B, N=N, d=d, K1=K1, n_sal=8, n_qm=10), k_div
+
+
+@pytest.mark.parametrize("seed", [11, 12, 13, 14, 15, 16])
+def test_stage1_diversity_set_shape_sweep(seed):
+    """Seeded shapes on the 256-row Gram path (N in [2048, 6000], rows of
+    16 bytes to 1.5 KB, B up to 4, any K_r:K_d split): scores against the
+    float64 oracle, pivots exactly the top-K_r of the kernel's own score,
+    the ascending union, a bit-exact gather, and every pick valid against
+    float64 distances to the GPU's own selected set."""
+    w, k_div = _sweep_case(seed)
+    print(f"[stage1-fps-sweep] seed={seed}: B={w.B} N={w.N} d={w.d} K1={w.K1} K_d={k_div}", flush=True)
+    inp = stage1_inputs(w)
+    cls = dev_tensor(inp["cls_logits"], w.dtype)
+    Z = dev_tensor(inp["vis_feats"], w.dtype)
+    T = dev_tensor(inp["text_emb"], w.dtype)
+    tl = torch.from_numpy(inp["text_len"]).cuda()
+    call = trevs.Prellm(cls, Z, T, tl, k_keep=w.K1, k_div=k_div, n_seg=w.n_seg,
+                        textual_ratio=w.rho, want_scores=True)
+    call()
+    torch.cuda.synchronize()
+    kept = call.kept_idx.cpu().numpy()
+    picks = call.div_idx.cpu().numpy()
+    feats = host_bits(call.kept_feats)
+    score = call.score.cpu().numpy()
+    K_r = w.K1 - k_div
+    o = run_oracle(inp, w)
+    assert_scores_close(score, o["score"], "s")
+    for b in range(w.B):
+        pivots = np.setdiff1d(kept[b], picks[b])
+        assert pivots.size == K_r and np.unique(picks[b]).size == k_div, b
+        assert np.array_equal(pivots, oracle.topk_ascending(score[b].astype(np.float64), K_r)), b
+        assert np.array_equal(kept[b], np.sort(np.concatenate([pivots, picks[b]]))), b
+        assert np.array_equal(feats[b], inp["vis_feats"][b][kept[b]]), b
+        check_fps_picks(oracle.to_f64(inp["vis_feats"][b], w.dtype), pivots, picks[b])
+
+
 def test_stage1_diversity_set_full_size_qwen(qwen_full):
     """The diversity set at the benchmarked shape (B=4, N=16384, d'=3584) with
     K_d = K1/4 = 1024 farthest-point tokens, the 3:1 split of Sec. 4.1 that
